@@ -1,0 +1,257 @@
+"""Absorbed-mode MLA decode with FP8 per-token content, BF16 RoPE and FP8 P blocks.
+
+Test infrastructure only (see the package docstring).  Everything here is
+float64 numpy, slow and literal.
+
+Notation (Section 2 absorbed score; Algorithm 1 inputs): one sequence, rows
+r = 0..R-1 (a row is one (query token, head) pair), cached tokens j = 0..N-1.
+
+  q8   uint8  [R, 512]  E4M3 codes of q_nope (absorbed query content part)
+  sq   f32    [R]       per-row query scale  (sigma_q)
+  qr   uint16 [R, 64]   bf16 bits of q_rope
+  c8   uint8  [N, 512]  E4M3 codes of the latent c_KV -- also the value operand
+  sk   f32    [N]       per-token latent scale (sigma_K = S_V)
+  kr   uint16 [N, 64]   bf16 bits of the RoPE key, stored unscaled
+  tau  float            softmax scale
+  visible int [R]       row r attends to tokens j < visible[r] (causal decode
+                        with several query tokens gives rows different limits)
+
+Restored logit (Section 2 absorbed score, content + RoPE terms; Section 3.1
+pre-scaled domain alignment -- here the alignment is written on the
+accumulator side, which is the same number in exact arithmetic):
+
+  s_rj = tau * ( sq_r * sk_j * sum_i D(q8_ri) D(c8_ji) + sum_i qr_ri kr_ji )
+
+The block size of the probability quantization is 64 tokens, aligned to
+absolute position 0 of the sequence (Section 3.2 (ii): BlockN = 64;
+Algorithm 1: B_c = 64).
+"""
+
+import numpy as np
+
+from . import e4m3
+from .quant import bf16_to_f32
+
+BLOCK = 64
+EPS = 2.0 ** -40
+FP8_MAX = 448.0
+
+
+def _f64(bits):
+    return bf16_to_f32(bits).astype(np.float64)
+
+
+def logits(q8, sq, qr, c8, sk, kr, tau):
+    """Restored logits s [R, N] in float64 (Section 2 absorbed score).
+
+    Products of decoded E4M3 values are exact in float64; the sums round in
+    float64 only.  Pinned through decode_none against a library attention
+    routine (tests/test_oracle_mla.py).
+    """
+    Q = e4m3.decode(q8)
+    C = e4m3.decode(c8)
+    content = Q @ C.T
+    rope = _f64(qr) @ _f64(kr).T
+    sq64 = np.asarray(sq, dtype=np.float64)
+    sk64 = np.asarray(sk, dtype=np.float64)
+    return tau * (sq64[:, None] * sk64[None, :] * content + rope)
+
+
+def _mask(s, visible, j0):
+    """Set s[r, j] = -inf where the absolute token index j0 + j >= visible[r]."""
+    n = s.shape[1]
+    idx = j0 + np.arange(n)
+    vis = np.asarray(visible)[:, None]
+    return np.where(idx[None, :] < vis, s, -np.inf)
+
+
+def decode_streaming(q8, sq, qr, c8, sk, kr, tau, visible, start=0, end=None):
+    """Appendix D / Algorithm 1, block by block, exactly as written, in float64.
+
+    Processes the tokens [start, end) (start a multiple of 64) in 64-token
+    blocks in increasing order (the monotone order of Appendix E).  Per row the
+    state is initialised as in Algorithm 1: m = -inf, sigma_p = 1, L = 0, O = 0.
+    For each block k:
+
+      m_k      = max(m_{k-1}, max_j s_j)                 online softmax
+      e_j      = exp(s_j - m_k)
+      et_j     = e_j * sk_j                              scale fusion, P' = P . S_V
+      sP_k     = max(max_j et_j / 448, EPS)              block-wise dynamic P quant
+      pi_j     = E4M3(et_j / sP_k)
+      gamma    = exp(m_{k-1} - m_k) * sP_{k-1} / sP_k
+      L_k      = gamma * L_{k-1} + sum_j e_j / sP_k      (unquantized normaliser)
+      O_k      = gamma * O_{k-1} + sum_j D(pi_j) D(c8_j) implicit dequantization
+
+    and finally o = O / L, LSE = m + ln(sigma_p * L) (Algorithm 1 finalisation).
+
+    A row with no visible token in a block skips that block (its state is left
+    unchanged); a row with no visible token at all returns o = 0, LSE = -inf.
+    Returns (o [R, 512] float64, lse [R] float64).
+    """
+    R = q8.shape[0]
+    N = c8.shape[0]
+    end = N if end is None else end
+    assert start % BLOCK == 0 and 0 <= start <= end <= N
+    m = np.full(R, -np.inf)
+    sp = np.ones(R)
+    L = np.zeros(R)
+    O = np.zeros((R, c8.shape[1]))
+    sk64 = np.asarray(sk, dtype=np.float64)
+    for j0 in range(start, end, BLOCK):
+        j1 = min(j0 + BLOCK, end)
+        s = _mask(logits(q8, sq, qr, c8[j0:j1], sk[j0:j1], kr[j0:j1], tau), visible, j0)
+        bmax = np.max(s, axis=1)
+        act = bmax > -np.inf
+        if not np.any(act):
+            continue
+        s = s[act]
+        m_new = np.maximum(m[act], bmax[act])
+        e = np.exp(s - m_new[:, None])
+        et = e * sk64[None, j0:j1]
+        sP = np.maximum(np.max(et, axis=1) / FP8_MAX, EPS)
+        pi = e4m3.encode(et / sP[:, None])
+        gamma = np.exp(m[act] - m_new) * sp[act] / sP
+        L[act] = gamma * L[act] + np.sum(e, axis=1) / sP
+        O[act] = gamma[:, None] * O[act] + e4m3.decode(pi) @ e4m3.decode(c8[j0:j1])
+        m[act] = m_new
+        sp[act] = sP
+    o = np.zeros_like(O)
+    lse = np.full(R, -np.inf)
+    ok = L > 0
+    o[ok] = O[ok] / L[ok, None]
+    lse[ok] = m[ok] + np.log(sp[ok] * L[ok])
+    return o, lse
+
+
+def decode_global(q8, sq, qr, c8, sk, kr, tau, visible, parts=False):
+    """The same quantity in closed form over the whole sequence (float64).
+
+    With M_r = max_j s_rj, e = exp(s - M), et = e * sk, per 64-token block k
+    sP_k = max(max_{j in k} et_j / 448, EPS) and pi = E4M3(et / sP_k):
+
+        o_r   = sum_k sP_rk * sum_{j in k} D(pi_rj) D(c8_j)  /  sum_j e_rj
+        LSE_r = M_r + ln sum_j e_rj
+
+    The P codes do not depend on the reference maximum (scaling a block by a
+    constant scales sP_k by the same constant) except through the EPS floor and
+    rounding, so this equals decode_streaming up to float64 rounding whenever no
+    contributing block sits on the floor.  If parts=True also returns a dict
+    with s, e, sP (per row and block), the quotients et/sP and the codes.
+    """
+    s = _mask(logits(q8, sq, qr, c8, sk, kr, tau), visible, 0)
+    R, N = s.shape
+    M = np.max(s, axis=1)
+    ok = M > -np.inf
+    Msafe = np.where(ok, M, 0.0)
+    e = np.where(np.isfinite(s), np.exp(s - Msafe[:, None]), 0.0)
+    et = e * np.asarray(sk, dtype=np.float64)[None, :]
+    nblk = (N + BLOCK - 1) // BLOCK
+    sP = np.zeros((R, nblk))
+    quot = np.zeros_like(et)
+    for k in range(nblk):
+        j0, j1 = k * BLOCK, min(N, (k + 1) * BLOCK)
+        sP[:, k] = np.maximum(np.max(et[:, j0:j1], axis=1) / FP8_MAX, EPS)
+        quot[:, j0:j1] = et[:, j0:j1] / sP[:, k:k + 1]
+    pi = e4m3.encode(quot)
+    w = e4m3.decode(pi) * np.repeat(sP, BLOCK, axis=1)[:, :N]     # sP_k * D(pi_j)
+    lam = np.sum(e, axis=1)
+    C = e4m3.decode(c8)
+    o = np.zeros((R, c8.shape[1]))
+    o[ok] = (w[ok] @ C) / lam[ok, None]
+    lse = np.full(R, -np.inf)
+    lse[ok] = M[ok] + np.log(lam[ok])
+    if parts:
+        return o, lse, dict(s=s, e=e, sP=sP, quot=quot, pi=pi, lam=lam, M=M)
+    return o, lse
+
+
+def decode_none(q8, sq, qr, c8, sk, kr, tau, visible):
+    """Special case without P quantization: softmax attention on the dequantized cache.
+
+    o_r = sum_j e_rj sk_j D(c8_j) / sum_j e_rj, LSE as in decode_global.  This is
+    textbook attention with keys [sk D(c8), kr], values sk D(c8) and queries
+    [sq D(q8), qr]; tests pin it against a library attention routine.
+    """
+    s = _mask(logits(q8, sq, qr, c8, sk, kr, tau), visible, 0)
+    M = np.max(s, axis=1)
+    ok = M > -np.inf
+    e = np.where(np.isfinite(s), np.exp(s - np.where(ok, M, 0.0)[:, None]), 0.0)
+    lam = np.sum(e, axis=1)
+    V = np.asarray(sk, dtype=np.float64)[:, None] * e4m3.decode(c8)
+    o = np.zeros((s.shape[0], c8.shape[1]))
+    o[ok] = (e[ok] @ V) / lam[ok, None]
+    lse = np.full(s.shape[0], -np.inf)
+    lse[ok] = M[ok] + np.log(lam[ok])
+    return o, lse
+
+
+def softmax_weights(q8, sq, qr, c8, sk, kr, tau, visible):
+    """Unquantized attention probabilities e / sum(e) [R, N] (float64)."""
+    s = _mask(logits(q8, sq, qr, c8, sk, kr, tau), visible, 0)
+    M = np.max(s, axis=1)
+    e = np.where(np.isfinite(s), np.exp(s - M[:, None]), 0.0)
+    return e / np.sum(e, axis=1, keepdims=True)
+
+
+def bf16_reference(qn, qr, ckv, kr, tau, visible):
+    """Unquantized reference: float64 attention on the bf16 inputs themselves.
+
+    s = tau (q_nope . c_KV + q_rope . k_rope), o = softmax(s) c_KV.  Used only
+    to report the error of the FP8 path against BF16 (Appendix G metrics).
+    """
+    s = tau * (_f64(qn) @ _f64(ckv).T + _f64(qr) @ _f64(kr).T)
+    s = _mask(s, visible, 0)
+    M = np.max(s, axis=1)
+    ok = M > -np.inf
+    e = np.where(np.isfinite(s), np.exp(s - np.where(ok, M, 0.0)[:, None]), 0.0)
+    lam = np.sum(e, axis=1)
+    o = np.zeros((s.shape[0], ckv.shape[1]))
+    o[ok] = (e[ok] @ _f64(ckv)) / lam[ok, None]
+    lse = np.full(s.shape[0], -np.inf)
+    lse[ok] = M[ok] + np.log(lam[ok])
+    return o, lse
+
+
+def combine(o_parts, lse_parts):
+    """Merge partial results of disjoint KV chunks by log-sum-exp.
+
+    LSE = log sum_i exp(LSE_i), o = sum_i exp(LSE_i - LSE) o_i.  Chunks whose
+    LSE is -inf contribute nothing; if every chunk is -inf the row is o = 0,
+    LSE = -inf.  (The paper's kernel returns o and the log-sum-exp per query,
+    Algorithm 1 finalisation, which is what makes this merge possible.)
+    """
+    o_parts = np.asarray(o_parts, dtype=np.float64)
+    lse_parts = np.asarray(lse_parts, dtype=np.float64)
+    M = np.max(lse_parts, axis=0)
+    ok = M > -np.inf
+    Ms = np.where(ok, M, 0.0)
+    w = np.where(np.isfinite(lse_parts), np.exp(lse_parts - Ms[None, :]), 0.0)
+    S = np.sum(w, axis=0)
+    o = np.zeros(o_parts.shape[1:])
+    o[ok] = np.einsum("pr,prd->rd", w[:, ok], o_parts[:, ok]) / S[ok, None]
+    lse = np.full(M.shape, -np.inf)
+    lse[ok] = Ms[ok] + np.log(S[ok])
+    return o, lse
+
+
+def decode_split(q8, sq, qr, c8, sk, kr, tau, visible, chunk):
+    """Split the sequence into chunks of `chunk` tokens (a multiple of 64), run
+    decode_streaming on each, and merge with combine."""
+    assert chunk % BLOCK == 0 and chunk > 0
+    N = c8.shape[0]
+    outs, lses = [], []
+    for a in range(0, max(N, 1), chunk):
+        o, l = decode_streaming(q8, sq, qr, c8, sk, kr, tau, visible, start=a, end=min(N, a + chunk))
+        outs.append(o)
+        lses.append(l)
+    return combine(outs, lses)
+
+
+def visible_counts(n_tokens, q_len, H, causal):
+    """Per-row visibility for one sequence of n_tokens (the q_len current tokens
+    included): row r = t * H + h may see tokens j < n_tokens - q_len + 1 + t when
+    causal, all n_tokens otherwise."""
+    t = np.repeat(np.arange(q_len), H)
+    if causal:
+        return n_tokens - q_len + 1 + t
+    return np.full(q_len * H, n_tokens)
