@@ -1,0 +1,194 @@
+/*
+ * snapmla.h -- C ABI of libsnapmla.so: FP8 Multi-head Latent Attention decode
+ * over a paged, per-token-quantized KV cache, for AMD Instinct MI355X (gfx950).
+ *
+ * The method is SnapMLA (arXiv 2602.10718):
+ *   - RoPE-aware per-token KV quantization (Section 3.1): the 512-d content
+ *     latent c_KV of every token is stored as OCP FP8 E4M3 with one float32
+ *     scale per token; the 64-d RoPE key stays BF16.
+ *   - Quantized PV pipeline reconstruction (Section 3.2, Appendix D): the
+ *     per-token V scale is fused into the probabilities, each 64-token block of
+ *     fused probabilities is quantized to E4M3 with its own dynamic scale, and
+ *     the online-softmax state is kept in the current block-scale domain
+ *     ("implicit dequantization").
+ *   - Fused token preparation (Section 3.3, Layer 1): quantize-on-append writes
+ *     new tokens straight into their paged slots; query quantization is fused
+ *     into the decode call.
+ * The split-KV log-sum-exp merge (snapmla_combine) uses the per-row
+ * log-sum-exp that Algorithm 1 returns next to the output.
+ *
+ * Conventions for every function:
+ *   - Every pointer argument is DEVICE memory owned by the caller unless noted;
+ *     the library allocates nothing and keeps no state besides a cached device
+ *     property record.  page_table, seq_lens and lse need 4-byte alignment;
+ *     every other pointer must be 16-byte aligned (SNAPMLA_MISALIGNED otherwise).
+ *   - Work is enqueued on `stream` (a hipStream_t; 0 is the legacy default
+ *     stream); calls return before the work runs.  Calls are thread-safe.
+ *   - The return value is a status code (SNAPMLA_OK == 0).  On failure nothing
+ *     is enqueued and snapmla_get_last_error() returns a message (thread-local).
+ *   - Data errors that need device data to detect (a page id outside
+ *     [0, num_pages), a sequence longer than max_pages * 64, or
+ *     0 < seq_len < q_len) never cause an out-of-bounds access: decode writes
+ *     NaN into every output row of that sequence and quantize_append skips the
+ *     token.
+ *
+ * Cache planes (one page = 64 consecutive tokens of one sequence):
+ *   kv_latent  uint8  [num_pages][64][512]   E4M3 codes of c_KV (also the value operand)
+ *   kv_scale   float  [num_pages][64]        per-token scale sigma_K (row = sigma_K * E4M3 codes)
+ *   k_rope     bf16   [num_pages][64][64]    RoPE key, stored unscaled (bit copy of the input)
+ *   page_table int32  [B][max_pages]         physical page of each 64-token logical page
+ *   seq_lens   int32  [B]                    tokens in the cache per sequence, INCLUDING the
+ *                                            tokens of the current step
+ * Queries:
+ *   q_nope  bf16 [B][q_len][H][512]   absorbed query content part (q^C W^UK, Section 2)
+ *   q_rope  bf16 [B][q_len][H][64]
+ * A "row" is one (query token t, head h) pair, row index t*H + h; a sequence
+ * has R = q_len*H rows.  With causal != 0 row t attends to the first
+ * seq_len - q_len + 1 + t tokens; otherwise every row attends to all seq_len.
+ */
+#ifndef SNAPMLA_H
+#define SNAPMLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SNAPMLA_ABI_VERSION 1
+
+enum snapmla_status {
+  SNAPMLA_OK = 0,
+  SNAPMLA_INVALID_ARGUMENT = 1,   /* a size, pointer or flag is out of range */
+  SNAPMLA_UNSUPPORTED = 2,        /* valid but not implemented (e.g. page_size != 64) */
+  SNAPMLA_WORKSPACE_TOO_SMALL = 3,
+  SNAPMLA_MISALIGNED = 4,         /* a pointer is not 16-byte aligned */
+  SNAPMLA_HIP_ERROR = 5           /* a HIP runtime call failed */
+};
+
+/* ABI version of the loaded library (SNAPMLA_ABI_VERSION). */
+int snapmla_abi_version(void);
+
+/* Message for the last failed call on this thread ("" if none).  The pointer
+ * stays valid until the next call on the same thread. */
+const char* snapmla_get_last_error(void);
+
+/*
+ * snapmla_quantize_append -- fused quantize-on-append (Section 3.3, Layer 1,
+ * Fused-K-Append; per-token granularity of Section 3.1 and Appendix C).
+ *
+ * For every sequence b and new token t < n_new, the token is written at
+ * position pos = seq_lens[b] - n_new + t of sequence b, i.e. into page
+ * page_table[b][pos / 64], slot pos % 64.  The latent row x (512 bf16) is
+ * quantized per token:
+ *     a = max_i |x_i|;  sigma = max(fp32(a / 448), 2^-40);  code_i = E4M3_rne(fp32(x_i / sigma))
+ * with IEEE float32 divisions, and sigma goes to kv_scale.  The RoPE row is
+ * copied bit for bit.  Tokens whose position is negative, beyond
+ * max_pages * 64, or whose page id is outside [0, num_pages) are skipped.
+ *
+ *   c_kv_new    bf16 [B][n_new][512]   device, read
+ *   k_rope_new  bf16 [B][n_new][64]    device, read
+ *   page_table  int32 [B][max_pages]   device, read
+ *   seq_lens    int32 [B]              device, read (already counting the new tokens)
+ *   page_size   must be 64 (SNAPMLA_UNSUPPORTED otherwise)
+ *   kv_latent, kv_scale, k_rope        device cache planes, written at the new slots only
+ * B >= 0, n_new >= 0 (B*n_new == 0 enqueues nothing), max_pages >= 1, num_pages >= 1.
+ */
+int snapmla_quantize_append(const void* c_kv_new, const void* k_rope_new,
+                            const int32_t* page_table, const int32_t* seq_lens,
+                            int32_t B, int32_t n_new, int32_t max_pages, int32_t num_pages,
+                            int32_t page_size,
+                            uint8_t* kv_latent, float* kv_scale, void* k_rope,
+                            hipStream_t stream);
+
+/*
+ * snapmla_quantize_rows -- the same per-row quantizer as above, dense: rows
+ * x[r][0..511] (bf16) -> codes[r][0..511] (E4M3) and scale[r] (float32).
+ * snapmla_decode applies it to q_nope (Section 3.3, Fused-Q-Quant; one query
+ * scale per row, Algorithm 1's sigma_q).  rows >= 0.
+ */
+int snapmla_quantize_rows(const void* x, int64_t rows, uint8_t* codes, float* scale,
+                          hipStream_t stream);
+
+/*
+ * Workspace for snapmla_decode / snapmla_combine, in bytes.  It holds the
+ * quantized queries, the split plan and, per KV piece, a float32 partial
+ * output [64*ceil(R/64)][512] and partial log-sum-exp.
+ *   kv_chunk_tokens == 0: balanced split over `num_splits` parts of the total
+ *                         64-token block count (num_splits >= 1; a sequence
+ *                         may span several parts and a part several sequences)
+ *   kv_chunk_tokens  > 0: every sequence is cut into chunks of kv_chunk_tokens
+ *                         (a multiple of 64); num_splits bounds the chunks per
+ *                         sequence (sequences needing more are flagged NaN)
+ * *bytes receives the size; returns SNAPMLA_INVALID_ARGUMENT on bad sizes.
+ */
+int snapmla_decode_workspace_size(int32_t B, int32_t q_len, int32_t H,
+                                  int32_t num_splits, int32_t kv_chunk_tokens,
+                                  size_t* bytes);
+
+/*
+ * snapmla_decode -- FP8 MLA decode over the paged cache (Algorithm 1 and
+ * Appendix D; Section 2 absorbed score).  Enqueues the query quantization and
+ * the decode kernel; the result is complete only after snapmla_combine.
+ *
+ * Per row r and cached token j the restored logit is
+ *     s = softmax_scale * ( sigma_q[r] * sigma_K[j] * <q8_r, c8_j> + <q_rope_r, k_rope_j> )
+ * (FP8 x FP8 content term, BF16 x BF16 RoPE term, both accumulated in float32).
+ * The tokens are visited in 64-token blocks in increasing order; per block:
+ * online softmax with running max m, e = exp(s - m); fused probabilities
+ * p' = e * sigma_K; block scale sigma_P = max(max p' / 448, 2^-40);
+ * codes pi = E4M3(p' / sigma_P); output and normalizer kept in the sigma_P
+ * domain (Appendix D recurrences); the PV product pi x c8 runs in FP8.
+ * Each KV piece (see snapmla_decode_workspace_size) writes its normalized
+ * partial output and log-sum-exp into the workspace.
+ *
+ *   q_nope, q_rope        bf16 queries (layout above), device, read
+ *   kv_latent, kv_scale, k_rope, page_table, seq_lens   cache (layout above), device, read
+ *   B >= 0; q_len in {1, 2}; H >= 1 with q_len*H <= 256
+ *   max_pages >= 1, num_pages >= 1, page_size == 64
+ *   softmax_scale         finite, > 0
+ *   causal                0 or 1 (only meaningful for q_len = 2)
+ *   num_splits, kv_chunk_tokens   split plan (see snapmla_decode_workspace_size)
+ *   workspace / workspace_bytes   device scratch of at least the queried size
+ */
+int snapmla_decode(const void* q_nope, const void* q_rope,
+                   const uint8_t* kv_latent, const float* kv_scale, const void* k_rope,
+                   const int32_t* page_table, const int32_t* seq_lens,
+                   int32_t B, int32_t q_len, int32_t H,
+                   int32_t max_pages, int32_t num_pages, int32_t page_size,
+                   float softmax_scale, int32_t causal,
+                   int32_t num_splits, int32_t kv_chunk_tokens,
+                   void* workspace, size_t workspace_bytes,
+                   hipStream_t stream);
+
+/*
+ * snapmla_combine -- split-KV log-sum-exp merge of the partial results that
+ * snapmla_decode left in `workspace` (same B, q_len, H, num_splits,
+ * kv_chunk_tokens and seq_lens as that call).  Per row:
+ *     LSE = log sum_i exp(LSE_i),  o = sum_i exp(LSE_i - LSE) o_i
+ * over the row's non-empty pieces.  A row that sees no token gets o = 0 and
+ * LSE = -inf; a sequence flagged by a data error gets NaN.
+ *
+ *   out        [B][q_len][H][512], bf16 (out_dtype 0, round to nearest even) or float32 (1)
+ *   lse        float32 [B][q_len][H], natural log of the sum of exp(s) (may be NULL)
+ */
+int snapmla_combine(const void* workspace, size_t workspace_bytes, const int32_t* seq_lens,
+                    int32_t B, int32_t q_len, int32_t H,
+                    int32_t num_splits, int32_t kv_chunk_tokens,
+                    void* out, int32_t out_dtype, float* lse,
+                    hipStream_t stream);
+
+/*
+ * snapmla_e4m3_encode -- test hook: E4M3 codes of n float32 values through the
+ * same device conversion the quantizers use (round to nearest even, values at
+ * or beyond 464 in magnitude saturate to +-448).  x, codes: device; n >= 0.
+ */
+int snapmla_e4m3_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SNAPMLA_H */

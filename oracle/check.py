@@ -1,0 +1,123 @@
+"""Reference results and acceptance bounds for checking a device decode against the oracle.
+
+Test infrastructure only (see the package docstring).  Inputs are raw bf16 bit
+patterns for one sequence; everything is recomputed here from the paper's
+definitions (quant, mla).
+
+Acceptance bounds.  The oracle evaluates the method exactly (float64); a
+device evaluates the same method in float32 arithmetic and, for the FP8
+products, in the matrix cores, whose accumulation aligns every group of 8
+consecutive products to the group's largest one and keeps about 13 bits below
+its leading bit (measured on gfx950: a product 2^-14 below the group maximum is
+dropped, one 2^-13 below is kept).  The bounds below propagate exactly these
+error sources; they contain no free tolerance besides float32 slack:
+
+  logit error   |ds_rj| <= delta_rj = tau*sigma_q*sigma_K * 7*2^-13 * sum_i |q8_ri c8_ji|
+                                      + tau * 2^-21 * sum_i |qr_ri kr_ji| + 2^-20 |s_rj|
+  LSE error     |dLSE_r| <= L*_r = log sum_j w_rj exp(delta_rj)       (w = softmax weights)
+  weight error  |dw_rj| <= w_rj (exp(delta_rj + L*_r) - 1)
+  P codes       a code may round the other way when its exact quotient lies within
+                the relative band (delta_rj + delta_r,argmax + 2^-20) of an E4M3
+                rounding midpoint ("ties"; either rounding is a correct result)
+  PV products   7*2^-13 * sum_j sP |D(pi_rj)| |D(c8_jd)| / Lambda_r  (same alignment window)
+
+so |do_rd| <= sum_j w'_rj-bound * |V_jd| + tie slack + PV window + 1e-5 * max|o_r|.
+"""
+
+import numpy as np
+
+from . import e4m3, mla, quant
+
+WINDOW = 2.0 ** -13
+
+
+def sequence_reference(qn, qr, ckv, kr, tau, q_len, H, causal, bf16=True):
+    """Oracle results for one sequence.
+
+    qn [q_len, H, 512] / qr [q_len, H, 64] / ckv [N, 512] / kr [N, 64]: uint16 bf16 bits.
+    Returns a dict with the quantized cache (codes, scales), the oracle output and
+    LSE (decode_global), its parts, and the unquantized BF16 reference.
+    """
+    R = q_len * H
+    qn = np.asarray(qn).reshape(R, 512)
+    qr = np.asarray(qr).reshape(R, 64)
+    q8, sq = quant.quantize_rows(qn)
+    c8, sk = quant.quantize_rows(ckv)
+    N = ckv.shape[0]
+    vis = mla.visible_counts(N, q_len, H, causal)
+    o, lse, parts = mla.decode_global(q8, sq, qr, c8, sk, kr, tau, vis, parts=True)
+    ref = dict(q8=q8, sq=sq, qr=qr, c8=c8, sk=sk, kr=kr, vis=vis, tau=tau, o=o, lse=lse, parts=parts)
+    if bf16:
+        ref["o_bf16"], ref["lse_bf16"] = mla.bf16_reference(qn, qr, ckv, kr, tau, vis)
+    return ref
+
+
+def bounds(ref):
+    """Per-element output bound [R, 512] and per-row LSE bound [R] (see module docstring)."""
+    q8, sq, qr, c8, sk, kr, tau = (ref[k] for k in ("q8", "sq", "qr", "c8", "sk", "kr", "tau"))
+    p = ref["parts"]
+    Q = np.abs(e4m3.decode(q8))
+    C = e4m3.decode(c8)
+    A = Q @ np.abs(C).T
+    rope = np.abs(quant.bf16_to_f32(qr).astype(np.float64)) @ np.abs(quant.bf16_to_f32(kr).astype(np.float64)).T
+    s = p["s"]
+    fin = np.isfinite(s)
+    delta = tau * (sq.astype(np.float64)[:, None] * sk.astype(np.float64)[None, :] * 7 * WINDOW * A
+                   + 2.0 ** -21 * rope) + 2.0 ** -20 * np.where(fin, np.abs(s), 0.0)
+    delta = np.where(fin, delta, 0.0)
+    lam = p["lam"]
+    ok = lam > 0
+    w = np.where(ok[:, None], p["e"] / np.where(ok, lam, 1.0)[:, None], 0.0)
+    Lstar = np.log(np.maximum(np.sum(w * np.exp(np.minimum(delta, 50.0)), axis=1), 1e-300))
+    Lstar = np.where(ok, Lstar, 0.0)
+    dw = w * np.expm1(np.minimum(delta + Lstar[:, None], 50.0))
+    V = np.abs(C) * sk.astype(np.float64)[:, None]
+    # the quantized weights differ from w by at most 2^-4 w (+ subnormal floor); bound |V| contributions by w(1+2^-3)
+    o_bound = dw @ V * (1 + 2.0 ** -3)
+    # ties of the probability codes
+    N = c8.shape[0]
+    nblk = p["sP"].shape[1]
+    quot = p["quot"]
+    vals = e4m3.finite_values()
+    mids = (vals[:-1] + vals[1:]) / 2
+    steps = vals[1:] - vals[:-1]
+    idx = np.clip(np.searchsorted(mids, quot), 0, len(mids) - 1)
+    idx2 = np.clip(idx - 1, 0, len(mids) - 1)
+    d1 = np.abs(quot - mids[idx])
+    d2 = np.abs(quot - mids[idx2])
+    near = np.where(d1 <= d2, idx, idx2)
+    dist = np.minimum(d1, d2) / np.maximum(mids[near], 1e-300)
+    # band: error of this token's logit plus that of its block's largest fused probability
+    et = p["e"] * sk.astype(np.float64)[None, :]
+    dblk = np.zeros_like(delta)
+    for k in range(nblk):
+        j0, j1 = 64 * k, min(N, 64 * k + 64)
+        am = j0 + np.argmax(et[:, j0:j1], axis=1)
+        dblk[:, j0:j1] = delta[np.arange(delta.shape[0]), am][:, None]
+    band = np.expm1(np.minimum(delta + dblk, 50.0)) + 2.0 ** -20
+    tie = (dist <= band) & (quot > 0)
+    sPfull = np.repeat(p["sP"], 64, axis=1)[:, :N]
+    tie_w = np.where(tie, sPfull * steps[near], 0.0) / np.where(ok, lam, 1.0)[:, None]
+    o_bound += tie_w @ np.abs(C)
+    # PV accumulation window
+    wq = e4m3.decode(p["pi"]) * sPfull / np.where(ok, lam, 1.0)[:, None]
+    o_bound += 7 * WINDOW * (np.abs(wq) @ np.abs(C))
+    o_bound += 1e-5 * np.max(np.abs(ref["o"]), axis=1, keepdims=True) + 1e-30
+    lse_bound = Lstar + 2.0 ** -20 * np.abs(np.where(np.isfinite(ref["lse"]), ref["lse"], 0.0)) + 1e-6
+    return o_bound, lse_bound, dict(delta=delta, Lstar=Lstar, tie_count=int(np.sum(tie)))
+
+
+def metrics(o_dev, lse_dev, o_ref, lse_ref):
+    """Appendix G style error metrics of o_dev against o_ref plus LSE difference."""
+    o_dev = np.asarray(o_dev, np.float64)
+    o_ref = np.asarray(o_ref, np.float64)
+    d = o_dev - o_ref
+    rel_l2 = float(np.linalg.norm(d) / max(np.linalg.norm(o_ref), 1e-300))
+    rmse = float(np.sqrt(np.mean(d ** 2)))
+    num = np.sum(o_dev * o_ref, axis=-1)
+    den = np.linalg.norm(o_dev, axis=-1) * np.linalg.norm(o_ref, axis=-1)
+    cos = np.where(den > 0, num / np.where(den > 0, den, 1), 1.0)
+    fin = np.isfinite(lse_ref)
+    lse_err = float(np.max(np.abs(np.asarray(lse_dev)[fin] - np.asarray(lse_ref)[fin]))) if np.any(fin) else 0.0
+    return dict(rel_l2=rel_l2, rmse=rmse, one_minus_cos=float(np.max(1 - cos)), max_abs=float(np.max(np.abs(d))),
+                lse_max_abs=lse_err)

@@ -1,0 +1,236 @@
+// C ABI of libsnapmla.so (declared in include/snapmla.h): argument validation,
+// workspace carve-up and kernel launches on the caller's stream.
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "snapmla.h"
+#include "snapmla_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return SNAPMLA_OK;
+}
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+bool misaligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) != 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(SNAPMLA_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
+}
+
+int check_shapes(int32_t B, int32_t q_len, int32_t H, int32_t num_splits, int32_t kv_chunk_tokens) {
+  if (B < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "B must be >= 0 (got %d)", B);
+  if (q_len != 1 && q_len != 2) return fail(SNAPMLA_INVALID_ARGUMENT, "q_len must be 1 or 2 (got %d)", q_len);
+  if (H < 1) return fail(SNAPMLA_INVALID_ARGUMENT, "H must be >= 1 (got %d)", H);
+  if ((int64_t)q_len * H > 256)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "q_len*H must be <= 256 (got %d)", q_len * H);
+  if (num_splits < 1) return fail(SNAPMLA_INVALID_ARGUMENT, "num_splits must be >= 1 (got %d)", num_splits);
+  if (kv_chunk_tokens < 0 || kv_chunk_tokens % 64 != 0)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "kv_chunk_tokens must be 0 or a positive multiple of 64 (got %d)",
+                kv_chunk_tokens);
+  return SNAPMLA_OK;
+}
+
+}  // namespace
+
+namespace snapmla {
+
+WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens) {
+  WsLayout L;
+  L.R = q_len * H;
+  L.G = (L.R + 63) / 64;
+  L.rows_pad = 64 * L.G;
+  L.pieces = kv_chunk_tokens == 0 ? num_splits + B : B * num_splits;
+  const size_t rows = (size_t)B * L.R;
+  size_t off = 0;
+  L.q8 = off;     off += align256(rows * 512);
+  L.sq = off;     off += align256(rows * 4);
+  L.prefix = off; off += align256(((size_t)B + 1) * 4);
+  L.flags = off;  off += align256((size_t)B * 4);
+  L.zero = off;   off += 1024;
+  L.lse = off;    off += align256((size_t)L.pieces * L.rows_pad * 4);
+  L.o = off;      off += align256((size_t)L.pieces * L.rows_pad * 512 * 4);
+  L.total = off;
+  return L;
+}
+
+}  // namespace snapmla
+
+extern "C" {
+
+int snapmla_abi_version(void) { return SNAPMLA_ABI_VERSION; }
+
+const char* snapmla_get_last_error(void) { return g_last_error.c_str(); }
+
+int snapmla_quantize_append(const void* c_kv_new, const void* k_rope_new, const int32_t* page_table,
+                            const int32_t* seq_lens, int32_t B, int32_t n_new, int32_t max_pages,
+                            int32_t num_pages, int32_t page_size, uint8_t* kv_latent, float* kv_scale,
+                            void* k_rope, hipStream_t stream) {
+  if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
+  if (B < 0 || n_new < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "B and n_new must be >= 0 (got %d, %d)", B, n_new);
+  if (max_pages < 1 || num_pages < 1)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
+  if ((int64_t)B * n_new == 0) return ok();
+  if (!c_kv_new || !k_rope_new || !page_table || !seq_lens || !kv_latent || !kv_scale || !k_rope)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(c_kv_new) || misaligned(k_rope_new) || misaligned4(page_table) || misaligned4(seq_lens) ||
+      misaligned(kv_latent) || misaligned(kv_scale) || misaligned(k_rope))
+    return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
+  return hip_status(snapmla::launch_append(static_cast<const uint16_t*>(c_kv_new),
+                                           static_cast<const uint16_t*>(k_rope_new), page_table, seq_lens, B,
+                                           n_new, max_pages, num_pages, kv_latent, kv_scale,
+                                           static_cast<uint16_t*>(k_rope), stream),
+                    "quantize_append launch");
+}
+
+int snapmla_quantize_rows(const void* x, int64_t rows, uint8_t* codes, float* scale, hipStream_t stream) {
+  if (rows < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "rows must be >= 0 (got %lld)", (long long)rows);
+  if (rows == 0) return ok();
+  if (!x || !codes || !scale) return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(x) || misaligned(codes) || misaligned(scale))
+    return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
+  return hip_status(snapmla::launch_quantize_rows(static_cast<const uint16_t*>(x), rows, codes, scale, stream),
+                    "quantize_rows launch");
+}
+
+int snapmla_e4m3_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t stream) {
+  if (n < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "n must be >= 0");
+  if (n == 0) return ok();
+  if (!x || !codes) return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(x) || misaligned(codes)) return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
+  return hip_status(snapmla::launch_encode(x, n, codes, stream), "e4m3_encode launch");
+}
+
+int snapmla_decode_workspace_size(int32_t B, int32_t q_len, int32_t H, int32_t num_splits,
+                                  int32_t kv_chunk_tokens, size_t* bytes) {
+  const int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (st != SNAPMLA_OK) return st;
+  if (!bytes) return fail(SNAPMLA_INVALID_ARGUMENT, "bytes must not be null");
+  *bytes = snapmla::ws_layout(B, q_len, H, num_splits, kv_chunk_tokens).total;
+  return ok();
+}
+
+int snapmla_decode(const void* q_nope, const void* q_rope, const uint8_t* kv_latent, const float* kv_scale,
+                   const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
+                   int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
+                   float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (st != SNAPMLA_OK) return st;
+  if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
+  if (max_pages < 1 || num_pages < 1)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(SNAPMLA_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
+  if (causal != 0 && causal != 1) return fail(SNAPMLA_INVALID_ARGUMENT, "causal must be 0 or 1");
+  if ((int64_t)max_pages * 64 > 0x7FFFFFFF) return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages too large");
+  const snapmla::WsLayout L = snapmla::ws_layout(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (B == 0) return ok();
+  if (!q_nope || !q_rope || !kv_latent || !kv_scale || !k_rope || !page_table || !seq_lens || !workspace)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(q_nope) || misaligned(q_rope) || misaligned(kv_latent) || misaligned(kv_scale) ||
+      misaligned(k_rope) || misaligned4(page_table) || misaligned4(seq_lens) || misaligned(workspace))
+    return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
+  if (workspace_bytes < L.total)
+    return fail(SNAPMLA_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes (got %zu)", L.total, workspace_bytes);
+
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  snapmla::PrepArgs p;
+  p.q_nope = static_cast<const uint16_t*>(q_nope);
+  p.q8 = ws + L.q8;
+  p.sq = reinterpret_cast<float*>(ws + L.sq);
+  p.rows = (int64_t)B * L.R;
+  p.seq_lens = seq_lens;
+  p.prefix = reinterpret_cast<int32_t*>(ws + L.prefix);
+  p.flags = reinterpret_cast<int32_t*>(ws + L.flags);
+  p.zero = ws + L.zero;
+  p.B = B;
+  p.q_len = q_len;
+  p.max_pages = max_pages;
+  p.chunk_blocks = kv_chunk_tokens / 64;
+  p.num_splits = num_splits;
+  hipError_t e = snapmla::launch_prep(p, stream);
+  if (e != hipSuccess) return hip_status(e, "decode prep launch");
+
+  snapmla::DecodeArgs d;
+  d.q8 = p.q8;
+  d.sq = p.sq;
+  d.q_rope = static_cast<const uint16_t*>(q_rope);
+  d.kv_latent = kv_latent;
+  d.kv_scale = kv_scale;
+  d.k_rope = static_cast<const uint16_t*>(k_rope);
+  d.page_table = page_table;
+  d.seq_lens = seq_lens;
+  d.prefix = p.prefix;
+  d.zero = p.zero;
+  d.part_o = reinterpret_cast<float*>(ws + L.o);
+  d.part_lse = reinterpret_cast<float*>(ws + L.lse);
+  d.B = B;
+  d.q_len = q_len;
+  d.H = H;
+  d.R = L.R;
+  d.G = L.G;
+  d.rows_pad = L.rows_pad;
+  d.max_pages = max_pages;
+  d.num_pages = num_pages;
+  d.causal = causal;
+  d.num_splits = num_splits;
+  d.chunk_blocks = kv_chunk_tokens / 64;
+  d.sl2 = softmax_scale * 1.4426950408889634f;
+  return hip_status(snapmla::launch_decode(d, stream), "decode launch");
+}
+
+int snapmla_combine(const void* workspace, size_t workspace_bytes, const int32_t* seq_lens, int32_t B,
+                    int32_t q_len, int32_t H, int32_t num_splits, int32_t kv_chunk_tokens, void* out,
+                    int32_t out_dtype, float* lse, hipStream_t stream) {
+  int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (st != SNAPMLA_OK) return st;
+  if (out_dtype != 0 && out_dtype != 1) return fail(SNAPMLA_INVALID_ARGUMENT, "out_dtype must be 0 or 1");
+  const snapmla::WsLayout L = snapmla::ws_layout(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (B == 0) return ok();
+  if (!workspace || !seq_lens || !out) return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(workspace) || misaligned4(seq_lens) || misaligned(out) || (lse && misaligned4(lse)))
+    return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
+  if (workspace_bytes < L.total)
+    return fail(SNAPMLA_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes (got %zu)", L.total, workspace_bytes);
+  const uint8_t* ws = static_cast<const uint8_t*>(workspace);
+  snapmla::CombineArgs c;
+  c.part_o = reinterpret_cast<const float*>(ws + L.o);
+  c.part_lse = reinterpret_cast<const float*>(ws + L.lse);
+  c.prefix = reinterpret_cast<const int32_t*>(ws + L.prefix);
+  c.flags = reinterpret_cast<const int32_t*>(ws + L.flags);
+  c.seq_lens = seq_lens;
+  c.out = out;
+  c.lse = lse;
+  c.B = B;
+  c.q_len = q_len;
+  c.H = H;
+  c.R = L.R;
+  c.rows_pad = L.rows_pad;
+  c.num_splits = num_splits;
+  c.chunk_blocks = kv_chunk_tokens / 64;
+  c.out_dtype = out_dtype;
+  return hip_status(snapmla::launch_combine(c, stream), "combine launch");
+}
+
+}  // extern "C"

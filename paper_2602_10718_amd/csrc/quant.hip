@@ -1,0 +1,162 @@
+// Per-token FP8 quantization kernels: dense rows (query quantization), the fused
+// quantize-on-append into paged slots, the split plan, and an E4M3 test hook.
+//
+// Per-token rule (Appendix C per-token quantization; Section 3.1 per-token
+// granularity for the content latent only; Algorithm 1's amax/448 scale rule):
+//   sigma = max(fp32(amax / 448), 2^-40),  code_i = E4M3_rne(fp32(x_i / sigma)).
+// Both divisions are IEEE float32 divisions (hipcc's default division is
+// correctly rounded), so codes and scales are reproducible bit for bit.
+
+#include "snapmla_device.h"
+#include "snapmla_internal.h"
+
+namespace snapmla {
+
+// One wave quantizes one 512-element bf16 row: lane l owns elements 8l..8l+7.
+__device__ __forceinline__ void quantize_row_wave(const uint16_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                  float* __restrict__ scale_out, int lane) {
+  const uint4 raw = reinterpret_cast<const uint4*>(src)[lane];
+  float x[8];
+  x[0] = bf16_to_f32(raw.x & 0xFFFFu); x[1] = bf16_to_f32(raw.x >> 16);
+  x[2] = bf16_to_f32(raw.y & 0xFFFFu); x[3] = bf16_to_f32(raw.y >> 16);
+  x[4] = bf16_to_f32(raw.z & 0xFFFFu); x[5] = bf16_to_f32(raw.z >> 16);
+  x[6] = bf16_to_f32(raw.w & 0xFFFFu); x[7] = bf16_to_f32(raw.w >> 16);
+  float a = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(x[i]));
+  a = wave_max(a);
+  const float sigma = fmaxf(a / kFp8Max, kEps);
+  float y[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) y[i] = clamp448(x[i] / sigma);
+  int w0 = cvt_pk_e4m3(y[0], y[1], 0, false);
+  w0 = cvt_pk_e4m3(y[2], y[3], w0, true);
+  int w1 = cvt_pk_e4m3(y[4], y[5], 0, false);
+  w1 = cvt_pk_e4m3(y[6], y[7], w1, true);
+  reinterpret_cast<uint2*>(dst)[lane] = make_uint2((uint32_t)w0, (uint32_t)w1);
+  if (lane == 0) *scale_out = sigma;
+}
+
+__global__ __launch_bounds__(256) void quantize_rows_kernel(const uint16_t* __restrict__ x, int64_t rows,
+                                                            uint8_t* __restrict__ codes,
+                                                            float* __restrict__ scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nw = (int64_t)gridDim.x * 4;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < rows; r += nw)
+    quantize_row_wave(x + r * kDc, codes + r * kDc, scale + r, lane);
+}
+
+// Fused-K-Append (Section 3.3, Layer 1): quantize each new token and write it,
+// with its unscaled bf16 RoPE row and its scale, into its paged slot.
+__global__ __launch_bounds__(256) void append_kernel(const uint16_t* __restrict__ c_kv_new,
+                                                     const uint16_t* __restrict__ k_rope_new,
+                                                     const int32_t* __restrict__ page_table,
+                                                     const int32_t* __restrict__ seq_lens, int B, int n_new,
+                                                     int max_pages, int num_pages, uint8_t* __restrict__ kv_latent,
+                                                     float* __restrict__ kv_scale, uint16_t* __restrict__ k_rope) {
+  const int lane = threadIdx.x & 63;
+  const int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tok >= (int64_t)B * n_new) return;
+  const int b = (int)(tok / n_new), t = (int)(tok % n_new);
+  const int pos = seq_lens[b] - n_new + t;
+  if (pos < 0 || pos >= max_pages * kPage) return;
+  const int page = page_table[(int64_t)b * max_pages + pos / kPage];
+  if (page < 0 || page >= num_pages) return;
+  const int64_t slot = (int64_t)page * kPage + (pos % kPage);
+  quantize_row_wave(c_kv_new + tok * kDc, kv_latent + slot * kDc, kv_scale + slot, lane);
+  if (lane < 8)
+    reinterpret_cast<uint4*>(k_rope + slot * kDr)[lane] = reinterpret_cast<const uint4*>(k_rope_new + tok * kDr)[lane];
+}
+
+__global__ __launch_bounds__(256) void encode_kernel(const float* __restrict__ x, int64_t n,
+                                                     uint8_t* __restrict__ codes) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i + 3 < n) {
+    const float4 v = *reinterpret_cast<const float4*>(x + i);
+    int w = cvt_pk_e4m3(clamp448(v.x), clamp448(v.y), 0, false);
+    w = cvt_pk_e4m3(clamp448(v.z), clamp448(v.w), w, true);
+    *reinterpret_cast<uint32_t*>(codes + i) = (uint32_t)w;
+  } else {
+    for (int64_t k = i; k < n; ++k) codes[k] = (uint8_t)(cvt_pk_e4m3(clamp448(x[k]), 0.0f, 0, false) & 0xFF);
+  }
+}
+
+// Query quantization (Fused-Q-Quant) over all rows, plus, in block 0, the split
+// plan: prefix[b] = number of 64-token blocks of valid sequences before b.
+__global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  if (blockIdx.x == 0) {
+    __shared__ int sums[256];
+    const int per = (a.B + 255) / 256;
+    const int b0 = tid * per, b1 = min(a.B, b0 + per);
+    int local = 0;
+    for (int b = b0; b < b1; ++b) {
+      const int n = a.seq_lens[b];
+      bool ok = (n == 0) || (n >= a.q_len && n <= a.max_pages * kPage);
+      const int nb = (n + kPage - 1) / kPage;
+      if (ok && a.chunk_blocks > 0) ok = (nb + a.chunk_blocks - 1) / a.chunk_blocks <= a.num_splits;
+      a.flags[b] = ok ? 0 : 1;
+      local += ok ? nb : 0;
+    }
+    sums[tid] = local;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {      // inclusive Hillis-Steele scan
+      const int v = tid >= off ? sums[tid - off] : 0;
+      __syncthreads();
+      sums[tid] += v;
+      __syncthreads();
+    }
+    int run = tid > 0 ? sums[tid - 1] : 0;
+    if (tid == 0) a.prefix[0] = 0;
+    for (int b = b0; b < b1; ++b) {
+      const int n = a.seq_lens[b];
+      run += a.flags[b] ? 0 : (n + kPage - 1) / kPage;
+      a.prefix[b + 1] = run;
+    }
+    reinterpret_cast<uint32_t*>(a.zero)[tid] = 0u;   // 256 threads x 4 B = 1 KiB
+    return;
+  }
+  const int64_t nw = (int64_t)(gridDim.x - 1) * 4;
+  for (int64_t r = (int64_t)(blockIdx.x - 1) * 4 + (tid >> 6); r < a.rows; r += nw)
+    quantize_row_wave(a.q_nope + r * kDc, a.q8 + r * kDc, a.sq + r, lane);
+}
+
+static int grid_for(int64_t waves) {
+  int64_t g = (waves + 3) / 4;
+  return (int)(g < 1 ? 1 : (g > 65535 ? 65535 : g));
+}
+
+hipError_t launch_quantize_rows(const uint16_t* x, int64_t rows, uint8_t* codes, float* scale,
+                                hipStream_t stream) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(quantize_rows_kernel, dim3(grid_for(rows)), dim3(256), 0, stream, x, rows, codes, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const uint16_t* c_kv_new, const uint16_t* k_rope_new, const int32_t* page_table,
+                         const int32_t* seq_lens, int B, int n_new, int max_pages, int num_pages,
+                         uint8_t* kv_latent, float* kv_scale, uint16_t* k_rope, hipStream_t stream) {
+  const int64_t toks = (int64_t)B * n_new;
+  if (toks <= 0) return hipSuccess;
+  const int64_t blocks = (toks + 3) / 4;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(append_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, c_kv_new, k_rope_new, page_table,
+                     seq_lens, B, n_new, max_pages, num_pages, kv_latent, kv_scale, k_rope);
+  return hipGetLastError();
+}
+
+hipError_t launch_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 1023) / 1024;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(encode_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, x, n, codes);
+  return hipGetLastError();
+}
+
+hipError_t launch_prep(const PrepArgs& a, hipStream_t stream) {
+  const int qblocks = a.rows > 0 ? grid_for(a.rows) : 0;
+  hipLaunchKernelGGL(prep_kernel, dim3(1 + qblocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace snapmla

@@ -1,0 +1,90 @@
+// Device-side building blocks shared by the SnapMLA kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace snapmla {
+
+// Shapes fixed by the method: 512-d content latent, 64-d RoPE part (Section 3.1:
+// eight content groups of 64 plus one RoPE group), 64-token pages that are also the
+// probability-quantization blocks (Section 3.2 (ii), BlockN = 64).
+constexpr int kDc = 512;
+constexpr int kDr = 64;
+constexpr int kPage = 64;
+constexpr float kFp8Max = 448.0f;
+// floor of every dynamic scale (Appendix D lower-bounds scales by a small epsilon)
+constexpr float kEps = 9.094947017729282e-13f;  // 2^-40
+
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef short v8s __attribute__((ext_vector_type(8)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v2i lds_v2i;
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// OCP E4M3 encode of two floats into bytes 0/1 (hi=false) or 2/3 (hi=true) of `old`.
+// The hardware conversion rounds to nearest even; inputs must stay below 464 in
+// magnitude (callers clamp where that is not guaranteed by construction).
+__device__ __forceinline__ int cvt_pk_e4m3(float a, float b, int old, bool hi) {
+  return hi ? __builtin_amdgcn_cvt_pk_fp8_f32(a, b, old, true)
+            : __builtin_amdgcn_cvt_pk_fp8_f32(a, b, old, false);
+}
+
+__device__ __forceinline__ float clamp448(float x) { return fminf(fmaxf(x, -kFp8Max), kFp8Max); }
+
+// 32x32x64 FP8 (E4M3 x E4M3) MFMA, float32 accumulate.  Lane (i%32, i/32) holds
+// A[i%32][32*(i/32) + 0..31] and B[32*(i/32) + 0..31][i%32]; C lane i register v is
+// C[8*(v/4) + 4*(i/32) + v%4][i%32].
+__device__ __forceinline__ v16f mfma_f8_32x32x64(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// 32x32x16 BF16 MFMA: lane (i%32, i/32) holds K = 8*(i/32) + 0..7; same C layout.
+__device__ __forceinline__ v16f mfma_bf16_32x32x16(v4i a, v4i b, v16f c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a),
+                                                 __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+}
+
+// Maximum / sum across the two 32-lane halves (lane i and lane i^32).
+__device__ __forceinline__ float xhalf_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// 16-byte (or 4-byte) global -> LDS copy: lane i writes its bytes at lds_base + i*size.
+__device__ __forceinline__ void g2lds16(const void* gptr, void* lds_base) {
+  __builtin_amdgcn_global_load_lds(gptr, lds_base, 16, 0, 0);
+}
+__device__ __forceinline__ void g2lds4(const void* gptr, void* lds_base) {
+  __builtin_amdgcn_global_load_lds(gptr, lds_base, 4, 0, 0);
+}
+
+__device__ __forceinline__ v2i lds_read_tr8(const uint8_t* p) {
+  return __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(p));
+}
+
+}  // namespace snapmla

@@ -1,0 +1,68 @@
+// Host-side launch interfaces between the C ABI (api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace snapmla {
+
+// Workspace carve-up shared by decode and combine.
+struct WsLayout {
+  int R = 0, G = 0, rows_pad = 0, pieces = 0;
+  size_t q8 = 0, sq = 0, prefix = 0, flags = 0, zero = 0, lse = 0, o = 0, total = 0;
+};
+WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens);
+
+struct PrepArgs {
+  const uint16_t* q_nope;   // [B*R][512]
+  uint8_t* q8;              // [B*R][512]
+  float* sq;                // [B*R]
+  int64_t rows;             // B*R
+  const int32_t* seq_lens;
+  int32_t* prefix;          // [B+1] cumulative 64-token block counts of valid sequences
+  int32_t* flags;           // [B] 1 = sequence rejected (data error)
+  uint8_t* zero;            // 1 KiB that the decode kernel reads in place of slots past a sequence end
+  int B, q_len, max_pages, chunk_blocks, num_splits;
+};
+
+struct DecodeArgs {
+  const uint8_t* q8;
+  const float* sq;
+  const uint16_t* q_rope;   // [B*R][64]
+  const uint8_t* kv_latent;
+  const float* kv_scale;
+  const uint16_t* k_rope;
+  const int32_t* page_table;
+  const int32_t* seq_lens;
+  const int32_t* prefix;
+  const uint8_t* zero;
+  float* part_o;            // [pieces][rows_pad][512]
+  float* part_lse;          // [pieces][rows_pad]
+  int B, q_len, H, R, G, rows_pad, max_pages, num_pages, causal;
+  int num_splits, chunk_blocks;  // chunk_blocks == 0: balanced plan over num_splits parts
+  float sl2;                     // softmax scale * log2(e)
+};
+
+struct CombineArgs {
+  const float* part_o;
+  const float* part_lse;
+  const int32_t* prefix;
+  const int32_t* flags;
+  const int32_t* seq_lens;
+  void* out;
+  float* lse;
+  int B, q_len, H, R, rows_pad, num_splits, chunk_blocks, out_dtype;
+};
+
+hipError_t launch_quantize_rows(const uint16_t* x, int64_t rows, uint8_t* codes, float* scale,
+                                hipStream_t stream);
+hipError_t launch_append(const uint16_t* c_kv_new, const uint16_t* k_rope_new, const int32_t* page_table,
+                         const int32_t* seq_lens, int B, int n_new, int max_pages, int num_pages,
+                         uint8_t* kv_latent, float* kv_scale, uint16_t* k_rope, hipStream_t stream);
+hipError_t launch_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t stream);
+hipError_t launch_prep(const PrepArgs& a, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+
+}  // namespace snapmla

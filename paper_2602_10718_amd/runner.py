@@ -1,0 +1,111 @@
+"""Device-side staging for a decode workload: cache planes, queries, workspace, and one step.
+
+A step is the whole hot path for one batch: quantize-and-append the step's new
+tokens, quantize the queries and decode (snapmla_decode), and merge the KV
+pieces (snapmla_combine).  Everything runs in libsnapmla.so; torch only owns
+the device buffers and the stream.
+"""
+
+import numpy as np
+import torch
+
+from . import snapmla as sm
+from .workloads import D_C, D_R, PAGE
+
+
+def _dev(a, dtype):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=dtype) if dtype is not None \
+        else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _u16_to_bf16(a):
+    """uint16 bit patterns (numpy) -> torch bfloat16 on the device, bit for bit."""
+    t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+    return t.view(torch.bfloat16)
+
+
+class DecodeRunner:
+    """Holds one workload's device buffers.
+
+    The cache is filled with snapmla_quantize_append (all tokens before the
+    step's n_new); step() appends the n_new step tokens, decodes and combines.
+    """
+
+    def __init__(self, wl, num_splits=None, kv_chunk_tokens=None, out_dtype=torch.float32, fill=True):
+        self.wl = wl
+        self.B, self.H, self.q_len = wl.B, wl.H, wl.q_len
+        self.kv_chunk_tokens = wl.kv_chunk_tokens if kv_chunk_tokens is None else kv_chunk_tokens
+        if num_splits is None:
+            if self.kv_chunk_tokens > 0:
+                num_splits = max(1, int(np.max((wl.seq_lens + self.kv_chunk_tokens - 1) // self.kv_chunk_tokens)))
+            else:
+                num_splits = sm.default_num_splits(self.q_len, self.H)
+        self.num_splits = num_splits
+        P = wl.num_pages
+        self.kv_latent = torch.zeros((P, PAGE, D_C), dtype=torch.uint8, device="cuda")
+        self.kv_scale = torch.zeros((P, PAGE), dtype=torch.float32, device="cuda")
+        self.k_rope = torch.zeros((P, PAGE, D_R), dtype=torch.bfloat16, device="cuda")
+        self.page_table = _dev(wl.page_table, torch.int32)
+        self.seq_lens = _dev(wl.seq_lens, torch.int32)
+        qn, qr = wl.queries()
+        self.q_nope = _u16_to_bf16(qn)
+        self.q_rope = _u16_to_bf16(qr)
+        ws = sm.snapmla_decode_workspace_size(self.B, self.q_len, self.H, self.num_splits, self.kv_chunk_tokens)
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device="cuda")
+        self.out = torch.empty((self.B, self.q_len, self.H, D_C), dtype=out_dtype, device="cuda")
+        self.lse = torch.empty((self.B, self.q_len, self.H), dtype=torch.float32, device="cuda")
+        # the step's new tokens (the last n_new of every sequence)
+        n_new = wl.n_new
+        ck = np.zeros((self.B, n_new, D_C), np.uint16)
+        kr = np.zeros((self.B, n_new, D_R), np.uint16)
+        for b in range(self.B):
+            N = int(wl.seq_lens[b])
+            lo = max(0, N - n_new)              # new token t lands at position N - n_new + t
+            if N > lo:
+                ck[b, lo - (N - n_new):], kr[b, lo - (N - n_new):] = wl.tokens(b, lo, N)
+        self.new_ckv = _u16_to_bf16(ck)
+        self.new_krope = _u16_to_bf16(kr)
+        if fill:
+            self.fill_prefix()
+
+    def fill_prefix(self, chunk=16384):
+        """Append every sequence's tokens before the step's new ones, in bulk."""
+        wl = self.wl
+        for b in range(self.B):
+            N = int(wl.seq_lens[b]) - wl.n_new
+            for t0 in range(0, max(N, 0), chunk):
+                t1 = min(N, t0 + chunk)
+                ck, kr = wl.tokens(b, t0, t1)
+                sm.snapmla_quantize_append(_u16_to_bf16(ck[None]), _u16_to_bf16(kr[None]),
+                                           self.page_table[b:b + 1].clone(),
+                                           torch.tensor([t1], dtype=torch.int32, device="cuda"),
+                                           wl.num_pages, self.kv_latent, self.kv_scale, self.k_rope)
+        torch.cuda.synchronize()
+
+    def append(self, stream=None):
+        sm.snapmla_quantize_append(self.new_ckv, self.new_krope, self.page_table, self.seq_lens, self.wl.num_pages,
+                                   self.kv_latent, self.kv_scale, self.k_rope, stream=stream)
+
+    def decode(self, stream=None):
+        sm.snapmla_decode(self.q_nope, self.q_rope, self.kv_latent, self.kv_scale, self.k_rope, self.page_table,
+                          self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits, self.kv_chunk_tokens,
+                          self.workspace, stream=stream)
+
+    def combine(self, stream=None):
+        sm.snapmla_combine(self.workspace, self.seq_lens, self.B, self.q_len, self.H, self.num_splits,
+                           self.kv_chunk_tokens, self.out, self.lse, stream=stream)
+
+    def step(self, stream=None):
+        self.append(stream)
+        self.decode(stream)
+        self.combine(stream)
+
+    def sequence_cache(self, b):
+        """(codes uint8 [N, 512], scales f32 [N], rope bits uint16 [N, 64]) of sequence b read back via the page table."""
+        N = int(self.wl.seq_lens[b])
+        npg = (N + PAGE - 1) // PAGE
+        pages = self.page_table[b, :npg].long()
+        codes = self.kv_latent[pages].reshape(-1, D_C)[:N].cpu().numpy()
+        scales = self.kv_scale[pages].reshape(-1)[:N].cpu().numpy()
+        rope = self.k_rope[pages].reshape(-1, D_R)[:N].view(torch.int16).cpu().numpy().view(np.uint16)
+        return codes, scales, rope

@@ -1,0 +1,143 @@
+"""ctypes binding of libsnapmla.so with the C function names (include/snapmla.h).
+
+Argument marshalling only: every computation runs in the HIP library.  Device
+buffers are torch tensors (used for allocation and streams); the current torch
+stream is passed as the hipStream_t.  Importing this module loads the library
+and raises if it has not been built.
+"""
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsnapmla.so")
+
+SNAPMLA_OK = 0
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "MISALIGNED",
+                5: "HIP_ERROR"}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_10718_amd.build` "
+                      "(or __graft_entry__.build())")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_p = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+_f32 = ctypes.c_float
+_sz = ctypes.c_size_t
+
+lib.snapmla_abi_version.restype = ctypes.c_int
+lib.snapmla_abi_version.argtypes = []
+lib.snapmla_get_last_error.restype = ctypes.c_char_p
+lib.snapmla_get_last_error.argtypes = []
+lib.snapmla_quantize_append.restype = ctypes.c_int
+lib.snapmla_quantize_append.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p]
+lib.snapmla_quantize_rows.restype = ctypes.c_int
+lib.snapmla_quantize_rows.argtypes = [_p, _i64, _p, _p, _p]
+lib.snapmla_decode_workspace_size.restype = ctypes.c_int
+lib.snapmla_decode_workspace_size.argtypes = [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
+lib.snapmla_decode.restype = ctypes.c_int
+lib.snapmla_decode.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
+                               _i32, _p, _sz, _p]
+lib.snapmla_combine.restype = ctypes.c_int
+lib.snapmla_combine.argtypes = [_p, _sz, _p, _i32, _i32, _i32, _i32, _i32, _p, _i32, _p, _p]
+lib.snapmla_e4m3_encode.restype = ctypes.c_int
+lib.snapmla_e4m3_encode.argtypes = [_p, _i64, _p, _p]
+
+EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
+           "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode"]
+
+
+class SnapMLAError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"snapmla status {status} ({STATUS_NAMES.get(status, '?')}): {msg}")
+        self.status = status
+
+
+def _check(status):
+    if status != SNAPMLA_OK:
+        raise SnapMLAError(status, lib.snapmla_get_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("snapmla buffers must be device tensors")
+    if not t.is_contiguous():
+        raise ValueError("snapmla buffers must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def snapmla_abi_version():
+    return lib.snapmla_abi_version()
+
+
+def snapmla_get_last_error():
+    return lib.snapmla_get_last_error().decode()
+
+
+def snapmla_quantize_append(c_kv_new, k_rope_new, page_table, seq_lens, num_pages, kv_latent, kv_scale, k_rope,
+                            page_size=64, stream=None):
+    """c_kv_new bf16 [B, n_new, 512], k_rope_new bf16 [B, n_new, 64], page_table int32 [B, max_pages],
+    seq_lens int32 [B]; writes into kv_latent uint8 [num_pages, 64, 512], kv_scale f32 [num_pages, 64],
+    k_rope bf16 [num_pages, 64, 64]."""
+    B, n_new = c_kv_new.shape[0], c_kv_new.shape[1]
+    _check(lib.snapmla_quantize_append(_ptr(c_kv_new), _ptr(k_rope_new), _ptr(page_table), _ptr(seq_lens), B, n_new,
+                                       page_table.shape[1], num_pages, page_size, _ptr(kv_latent), _ptr(kv_scale),
+                                       _ptr(k_rope), _stream(stream)))
+
+
+def snapmla_quantize_rows(x, codes, scale, stream=None):
+    """x bf16 [rows, 512] -> codes uint8 [rows, 512], scale f32 [rows]."""
+    _check(lib.snapmla_quantize_rows(_ptr(x), x.numel() // 512, _ptr(codes), _ptr(scale), _stream(stream)))
+
+
+def snapmla_e4m3_encode(x, codes, stream=None):
+    _check(lib.snapmla_e4m3_encode(_ptr(x), x.numel(), _ptr(codes), _stream(stream)))
+
+
+def snapmla_decode_workspace_size(B, q_len, H, num_splits, kv_chunk_tokens):
+    out = _sz(0)
+    _check(lib.snapmla_decode_workspace_size(B, q_len, H, num_splits, kv_chunk_tokens, ctypes.byref(out)))
+    return out.value
+
+
+def snapmla_decode(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, softmax_scale, causal,
+                   num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None):
+    """q_nope bf16 [B, q_len, H, 512], q_rope bf16 [B, q_len, H, 64]; cache planes as in snapmla_quantize_append;
+    workspace uint8 of at least snapmla_decode_workspace_size(...) bytes."""
+    B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
+    _check(lib.snapmla_decode(_ptr(q_nope), _ptr(q_rope), _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope),
+                              _ptr(page_table), _ptr(seq_lens), B, q_len, H, page_table.shape[1], kv_latent.shape[0],
+                              page_size, float(softmax_scale), int(causal), num_splits, kv_chunk_tokens,
+                              _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def snapmla_combine(workspace, seq_lens, B, q_len, H, num_splits, kv_chunk_tokens, out, lse=None, stream=None):
+    """out bf16 or f32 [B, q_len, H, 512]; lse f32 [B, q_len, H] or None."""
+    if out.dtype == torch.float32:
+        od = 1
+    elif out.dtype == torch.bfloat16:
+        od = 0
+    else:
+        raise ValueError("out must be bfloat16 or float32")
+    _check(lib.snapmla_combine(_ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(seq_lens), B,
+                               q_len, H, num_splits, kv_chunk_tokens, _ptr(out), od, _ptr(lse), _stream(stream)))
+
+
+def default_num_splits(q_len, H, device=None):
+    """One workgroup per compute unit across all row groups, rounded down to a multiple of 8."""
+    props = torch.cuda.get_device_properties(device if device is not None else torch.cuda.current_device())
+    groups = math.ceil(q_len * H / 64)
+    return max(8, (props.multi_processor_count // groups) // 8 * 8)

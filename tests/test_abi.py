@@ -1,0 +1,103 @@
+"""Host-only checks of the C ABI: the library loads, exports what include/snapmla.h declares,
+and rejects bad arguments with the documented status codes before touching the GPU."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "snapmla.h")
+LIB = os.path.join(ROOT, "paper_2602_10718_amd", "libsnapmla.so")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(snapmla_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def sm():
+    if not os.path.exists(LIB):
+        pytest.fail("libsnapmla.so is not built (run __graft_entry__.build())")
+    from paper_2602_10718_amd import snapmla
+    return snapmla
+
+
+def test_every_declared_symbol_is_exported(sm):
+    names = _declared()
+    assert len(names) >= 8
+    lib = ctypes.CDLL(LIB)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in snapmla.h but not exported"
+    assert set(names) == set(sm.EXPORTS)
+
+
+def test_abi_version(sm):
+    assert sm.snapmla_abi_version() == 1
+
+
+def test_workspace_size_layout(sm):
+    a = sm.snapmla_decode_workspace_size(64, 1, 64, 256, 0)
+    b = sm.snapmla_decode_workspace_size(64, 1, 64, 256, 4096)
+    assert a > 64 * 64 * (512 + 4) and b > a
+    # partial outputs dominate: (parts + B) x 64 rows x 512 floats
+    assert a >= (256 + 64) * 64 * 512 * 4
+
+
+@pytest.mark.parametrize("args,status", [
+    ((-1, 1, 64, 8, 0), 1),      # B < 0
+    ((4, 3, 64, 8, 0), 1),       # q_len not in {1, 2}
+    ((4, 1, 0, 8, 0), 1),        # H < 1
+    ((4, 2, 129, 8, 0), 1),      # q_len*H > 256
+    ((4, 1, 64, 0, 0), 1),       # num_splits < 1
+    ((4, 1, 64, 8, 100), 1),     # chunk not a multiple of 64
+])
+def test_workspace_size_rejects(sm, args, status):
+    out = ctypes.c_size_t(0)
+    assert sm.lib.snapmla_decode_workspace_size(*args, ctypes.byref(out)) == status
+    assert sm.snapmla_get_last_error() != ""
+
+
+def test_decode_argument_errors_before_any_launch(sm):
+    L = sm.lib
+    # unsupported page size
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, None, 0, None)
+    assert st == 2
+    # bad softmax scale
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, float("nan"), 0, 8, 0, None, 0,
+                          None)
+    assert st == 1
+    # null pointers
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0, None)
+    assert st == 1 and "null" in sm.snapmla_get_last_error()
+    # misaligned pointer (never dereferenced: validation fails first)
+    p = 16 * 1024 + 8
+    st = L.snapmla_decode(p, p, p, p, p, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096, 1 << 30, None)
+    assert st == 4
+    # workspace too small
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096, 16, None)
+    assert st == 3
+    # causal flag
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 7, 8, 0, 4096, 1 << 30,
+                          None)
+    assert st == 1
+    # empty batch is a no-op
+    assert L.snapmla_decode(None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+                            None) == 0
+
+
+def test_other_entry_points_validate(sm):
+    L = sm.lib
+    assert L.snapmla_quantize_append(None, None, None, None, 1, 1, 4, 4, 32, None, None, None, None) == 2
+    assert L.snapmla_quantize_append(None, None, None, None, -1, 1, 4, 4, 64, None, None, None, None) == 1
+    assert L.snapmla_quantize_append(None, None, None, None, 0, 1, 4, 4, 64, None, None, None, None) == 0
+    assert L.snapmla_quantize_append(None, None, None, None, 2, 1, 4, 4, 64, None, None, None, None) == 1
+    assert L.snapmla_quantize_rows(None, -1, None, None, None) == 1
+    assert L.snapmla_quantize_rows(None, 0, None, None, None) == 0
+    assert L.snapmla_quantize_rows(4100, 4, 4096, 4096, None) == 4
+    assert L.snapmla_e4m3_encode(None, 5, None, None) == 1
+    assert L.snapmla_combine(None, 0, None, 2, 1, 16, 8, 0, None, 3, None, None) == 1
+    assert L.snapmla_combine(4096, 16, 4096, 2, 1, 16, 8, 0, 4096, 0, None, None) == 3

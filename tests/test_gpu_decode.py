@@ -1,0 +1,130 @@
+"""GPU: decode + combine against the oracle, edge cases, bitwise invariances."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2602_10718_amd import workloads as wl
+from gpu_common import runner, reference, check_sequence
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(w, **kw):
+    r = runner(w, **kw)
+    r.step()
+    torch.cuda.synchronize()
+    return r
+
+
+CASES = {
+    # name: (workload factory, runner kwargs)
+    "tiny-cfg1": (lambda: wl.make(1), dict(num_splits=8)),
+    "ragged-h16": (lambda: wl.custom(B=4, H=16, q_len=1, seq_lens=[1, 63, 64, 517], seed=21), dict(num_splits=16)),
+    "ragged-h64-rotary": (lambda: wl.custom(B=3, H=64, q_len=1, seq_lens=[700, 129, 1000], sigma_tok=1.5,
+                                            rotary=True, seed=22), dict(num_splits=24)),
+    "h128-two-rowgroups": (lambda: wl.custom(B=2, H=128, q_len=1, seq_lens=[300, 450], seed=23), dict(num_splits=8)),
+    "mtp-causal-r256": (lambda: wl.custom(B=3, H=128, q_len=2, seq_lens=[2, 65, 257], causal=True, seed=24,
+                                          n_new=2), dict(num_splits=8)),
+    "mtp-causal-h32": (lambda: wl.custom(B=2, H=32, q_len=2, seq_lens=[129, 64], causal=True, seed=25, n_new=2),
+                       dict(num_splits=5)),
+    "more-parts-than-blocks": (lambda: wl.custom(B=2, H=16, q_len=1, seq_lens=[100, 30], seed=26),
+                               dict(num_splits=64)),
+    "one-part": (lambda: wl.custom(B=3, H=64, q_len=1, seq_lens=[200, 64, 333], seed=27), dict(num_splits=1)),
+    "fixed-chunks": (lambda: wl.custom(B=3, H=64, q_len=1, seq_lens=[1000, 64, 129], seed=28),
+                     dict(num_splits=8, kv_chunk_tokens=128)),
+    "fixed-chunks-causal": (lambda: wl.custom(B=2, H=64, q_len=2, seq_lens=[513, 66], causal=True, seed=29, n_new=2),
+                            dict(num_splits=3, kv_chunk_tokens=192)),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_decode_matches_oracle(name):
+    fac, kw = CASES[name]
+    w = fac()
+    run = _run(w, **kw)
+    qn, qr = w.queries()
+    for b in range(w.B):
+        ref = reference(w, b, qn, qr)
+        check_sequence(run, b, ref, label=name)
+
+
+def test_tame_data_tight_agreement():
+    """Small logits: the derived bounds shrink to ~1e-4 and the output must follow them."""
+    w = wl.custom(B=2, H=64, q_len=1, seq_lens=[777, 300], sigma_tok=0.2, seed=31)
+    run = _run(w, num_splits=16)
+    qn, qr = w.queries()
+    qn = wl.f32_to_bf16_bits(wl.bf16_bits_to_f32(qn) * np.float32(0.05))   # shrink the content logits
+    run.q_nope.copy_(torch.from_numpy(qn.view(np.int16)).cuda().view(torch.bfloat16))
+    run.decode()
+    run.combine()
+    torch.cuda.synchronize()
+    for b in range(w.B):
+        m = check_sequence(run, b, reference(w, b, qn, qr), label="tame")
+        assert m["rel_l2"] < 2e-3 and m["lse_max_abs"] < 1e-3
+
+
+def test_empty_and_invalid_sequences():
+    w = wl.custom(B=5, H=16, q_len=2, seq_lens=[0, 130, 70, 1, 64], causal=True, seed=32, n_new=0)
+    run = runner(w, num_splits=8)
+    # sequence 1: a page id out of range -> NaN rows; sequence 3 has 0 < seq_len < q_len -> NaN
+    pt = run.page_table.clone()
+    pt[1, 1] = w.num_pages + 3
+    run.page_table = pt
+    run.decode()
+    run.combine()
+    torch.cuda.synchronize()
+    out = run.out.cpu().numpy()
+    lse = run.lse.cpu().numpy()
+    assert np.all(out[0] == 0) and np.all(lse[0] == -np.inf)
+    assert np.all(np.isnan(out[1])) and np.all(np.isnan(lse[1]))
+    assert np.all(np.isnan(out[3])) and np.all(np.isnan(lse[3]))
+    qn, qr = w.queries()
+    for b in (2, 4):
+        check_sequence(run, b, reference(w, b, qn, qr), label="empty-invalid")
+    # a sequence longer than max_pages * 64 is rejected
+    seq = run.seq_lens.clone()
+    seq[2] = 64 * w.max_pages + 1
+    run.seq_lens = seq
+    run.decode()
+    run.combine()
+    torch.cuda.synchronize()
+    assert np.all(np.isnan(run.out[2].cpu().numpy()))
+    assert np.isfinite(run.out[4].cpu().numpy()).all()
+
+
+def test_page_shuffle_and_rerun_are_bitwise_identical():
+    w1 = wl.custom(B=3, H=64, q_len=1, seq_lens=[500, 64, 1111], seed=33, shuffle_pages=False)
+    w2 = wl.custom(B=3, H=64, q_len=1, seq_lens=[500, 64, 1111], seed=33, shuffle_pages=True)
+    assert not np.array_equal(w1.page_table, w2.page_table)
+    r1 = _run(w1, num_splits=12)
+    r2 = _run(w2, num_splits=12)
+    o1 = r1.out.clone()
+    assert torch.equal(o1.view(torch.int32), r2.out.view(torch.int32))
+    assert torch.equal(r1.lse.view(torch.int32), r2.lse.view(torch.int32))
+    r1.decode()
+    r1.combine()
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int32), r1.out.view(torch.int32))
+
+
+def test_split_plans_agree():
+    """Different split plans give the same result up to float32 merge rounding."""
+    w = wl.custom(B=3, H=64, q_len=1, seq_lens=[2000, 640, 3001], seed=34)
+    outs = []
+    for kw in (dict(num_splits=1), dict(num_splits=7), dict(num_splits=40), dict(num_splits=50, kv_chunk_tokens=64)):
+        r = _run(w, **kw)
+        outs.append((r.out.cpu().numpy().astype(np.float64), r.lse.cpu().numpy().astype(np.float64)))
+    o0, l0 = outs[0]
+    for o, l in outs[1:]:
+        assert np.linalg.norm(o - o0) / np.linalg.norm(o0) < 1e-5
+        assert np.max(np.abs(l - l0)) < 1e-4
+
+
+def test_bf16_output():
+    w = wl.custom(B=2, H=16, q_len=1, seq_lens=[300, 100], seed=35)
+    r32 = _run(w, num_splits=8)
+    r16 = _run(w, num_splits=8, out_dtype=torch.bfloat16)
+    assert torch.equal(r32.out.to(torch.bfloat16).view(torch.int16), r16.out.view(torch.int16))
