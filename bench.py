@@ -1,0 +1,186 @@
+"""Benchmark of the SnapMLA FP8 MLA decode hot path on one MI355X.
+
+One step = the whole hot path for one batch: quantize-and-append the step's new
+tokens into the paged FP8 cache, quantize the queries, decode every sequence
+(FP8 QK + BF16 RoPE, online softmax, fused/quantized P, FP8 PV), and merge the
+split-KV pieces.  Inputs are resident in HBM before timing starts.
+
+Default workload: 64-head MLA decode, batch 64, one query token, ragged context
+lengths uniform in [8192, 32768], 64-token pages in shuffled physical order.
+
+Prints ONE JSON line.  `value` is the achieved KV-cache read rate
+(sum of context lengths x 644 B per token / step time), i.e. the metric's
+"achieved KV HBM GB/s"; `us_per_step` is the step time.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MLA decode µs/step + achieved KV HBM GB/s (% of peak), 64 heads, 32K ctx"
+HBM_PEAK_GBPS = 8000.0
+BYTES_PER_TOKEN = 512 + 2 * 64 + 4           # e4m3 latent + bf16 rope + f32 scale
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
+
+
+def _src_hash():
+    h = hashlib.sha256()
+    for f in ("decode.hip", "snapmla_device.h"):
+        h.update(open(os.path.join(ROOT, "paper_2602_10718_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def _traffic(workload_name):
+    """HBM bytes per decode launch measured with rocprofv3 counters (profiles/), if still current."""
+    try:
+        d = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    e = d.get(workload_name)
+    if not e or e.get("src_hash") != _src_hash():
+        return None
+    return e.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, budget_s=15.0):
+    """The oracle (float64 numpy, as written) on a bounded sample of the same workload."""
+    import numpy as np
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    from oracle import mla, quant
+    qn, qr = w.queries()
+    el = 0.0          # oracle compute time only (input generation excluded)
+    toks = 0
+    seqs = 0
+    for b in range(w.B):
+        N = int(w.seq_lens[b])
+        ck, kr = w.tokens(b, 0, N)
+        ts = time.perf_counter()
+        q8, sq = quant.quantize_rows(qn[b].reshape(-1, 512))
+        c8, sk = quant.quantize_rows(ck)
+        vis = mla.visible_counts(N, w.q_len, w.H, w.causal)
+        mla.decode_streaming(q8, sq, qr[b].reshape(-1, 64), c8, sk, kr, w.tau, vis)
+        el += time.perf_counter() - ts
+        toks += N
+        seqs += 1
+        if el > budget_s and seqs >= 2:
+            break
+    return {"value": toks * BYTES_PER_TOKEN / el / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{seqs} of {w.B} sequences ({toks} KV tokens, {w.H * w.q_len} rows each), quantize + "
+                      f"decode_streaming; {el:.1f} s; full step extrapolated "
+                      f"{el * w.total_tokens / toks * 1e6:.0f} us"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3, help="workload 1..5 (3 is the headline)")
+    ap.add_argument("--num-splits", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the decode path shards by "
+              "sequence / head / KV chunk without collectives; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2602_10718_amd import workloads as wl
+    from paper_2602_10718_amd.runner import DecodeRunner
+
+    torch.cuda.set_device(0)
+    w = wl.make(args.config)
+    t_fill = time.perf_counter()
+    run = DecodeRunner(w, num_splits=args.num_splits, out_dtype=torch.bfloat16)
+    t_fill = time.perf_counter() - t_fill
+    print(f"[bench] cache filled ({w.total_tokens} tokens) in {t_fill:.1f} s", file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        run.step()
+    torch.cuda.synchronize()
+
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        run.step()
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / args.steps
+
+    # per-call durations over the same number of steps (events on the launch stream)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        run.append()
+        ev[k][1].record(stream)
+        run.decode()
+        ev[k][2].record(stream)
+        run.combine()
+        ev[k][3].record(stream)
+    torch.cuda.synchronize()
+    append_us = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
+    decode_us = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) * 1e3
+    combine_us = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
+
+    print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
+    kv_bytes = w.kv_bytes()
+    gbps = kv_bytes / (ms_per_step * 1e-3) / 1e9
+    decode_gbps = kv_bytes / (decode_us * 1e-6) / 1e9
+    traffic = _traffic(w.name)
+    line = {
+        "metric": METRIC,
+        "value": round(gbps, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "us_per_step": round(ms_per_step * 1e3, 1),
+        "frac_of_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "e4m3",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.CONFIG_NAMES[args.config],
+            "batch": w.B, "heads": w.H, "q_len": w.q_len, "causal": bool(w.causal),
+            "ctx_min": int(w.seq_lens.min()), "ctx_max": int(w.seq_lens.max()),
+            "kv_tokens": w.total_tokens, "kv_bytes": kv_bytes, "page": 64,
+            "num_splits": run.num_splits, "kv_chunk_tokens": run.kv_chunk_tokens,
+            "append_per_step": w.n_new,
+        },
+        "breakdown_us": {"append": round(append_us, 2), "decode": round(decode_us, 2),
+                         "combine": round(combine_us, 2)},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "snapmla_decode (query-quantization/plan kernel + decode kernel)",
+            "achieved": round(decode_gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(decode_gbps / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": kv_bytes,
+        },
+        "cache_fill_s": round(t_fill, 1),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
