@@ -75,13 +75,39 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// 16-byte (or 4-byte) global -> LDS copy: lane i writes its bytes at lds_base + i*size.
+// Workgroup barrier that waits only for what the caller names: the vector-memory
+// counter down to VM (direct-to-LDS copies still in flight may stay in flight)
+// and all LDS operations of this wave.  The empty asm statements keep the
+// compiler from moving memory accesses across the barrier.  (__syncthreads()
+// would also drain every outstanding direct-to-LDS copy.)
+template <int VM>
+__device__ __forceinline__ void barrier_vm_lgkm0() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 16-byte (or 4-byte) global -> LDS copy: lane i writes its bytes at lds_base + i*size
+// (lds_base must be wave-uniform).  Written as inline assembly on purpose: the
+// compiler's own form of this instruction makes it drain every outstanding copy
+// before each later LDS transpose read (it cannot tell which LDS bytes a copy
+// writes).  The kernels wait for these copies explicitly with s_waitcnt vmcnt.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)((__attribute__((address_space(3))) const uint8_t*)p);
+}
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void g2lds16(const void* gptr, void* lds_base) {
-  __builtin_amdgcn_global_load_lds(gptr, lds_base, 16, 0, 0);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_offset(lds_base))), "v"(gptr) : "memory", "m0");
 }
 __device__ __forceinline__ void g2lds4(const void* gptr, void* lds_base) {
-  __builtin_amdgcn_global_load_lds(gptr, lds_base, 4, 0, 0);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_offset(lds_base))), "v"(gptr) : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 __device__ __forceinline__ v2i lds_read_tr8(const uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(p));
