@@ -107,7 +107,25 @@ __device__ __forceinline__ void g2lds4(const void* gptr, void* lds_base) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
                :: "s"(__builtin_amdgcn_readfirstlane(lds_offset(lds_base))), "v"(gptr) : "memory", "m0");
 }
+// Same copies addressed as a wave-uniform 64-bit base (SGPRs) plus a per-lane
+// 32-bit byte offset, so the address costs no vector instructions.
+__device__ __forceinline__ void g2lds16_so(const void* sbase, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_off)), "v"(voff), "s"(sbase) : "memory", "m0");
+}
+__device__ __forceinline__ void g2lds4_so(const void* sbase, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds_off)), "v"(voff), "s"(sbase) : "memory", "m0");
+}
 #pragma clang diagnostic pop
+
+// Returns x unchanged but opaque to the optimiser, so that per-iteration address
+// arithmetic is not hoisted out of a software-pipelined loop (where the hoisted
+// values would only be spilled).
+__device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
 
 __device__ __forceinline__ v2i lds_read_tr8(const uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(p));

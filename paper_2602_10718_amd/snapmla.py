@@ -13,7 +13,7 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsnapmla.so")
+LIB_PATH = os.environ.get("SNAPMLA_LIB") or os.path.join(_HERE, "libsnapmla.so")
 
 SNAPMLA_OK = 0
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "MISALIGNED",
