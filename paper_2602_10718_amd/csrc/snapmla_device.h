@@ -130,5 +130,9 @@ __device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
 __device__ __forceinline__ v2i lds_read_tr8(const uint8_t* p) {
   return __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(p));
 }
+// Same read addressed by a 32-bit LDS byte address.
+__device__ __forceinline__ v2i lds_read_tr8_at(uint32_t lds_addr) {
+  return __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(uintptr_t)lds_addr);
+}
 
 }  // namespace snapmla
