@@ -354,11 +354,9 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     };
     // Copies per PV wave and page: 8 latent instructions, then 2 RoPE + 1 scale
     // instruction, addressed by a wave-uniform base and the per-lane offsets above.
-    // Schedule: the latent of block j is copied at the end of period j-3 (its stage
-    // held block j-4, whose PV product has just finished), the RoPE/scale part at
-    // the top of period j-2 (its stage held block j-3, read by the QK waves in the
-    // previous period).  After the global stores that end a piece the latent copy
-    // moves to the next period's top (the barrier there drains every access).
+    // Block j is copied right after the barrier that opens period j-2: its latent
+    // stage held block j-4 (PV product done in period j-3) and its RoPE/scale stage
+    // block j-3 (read by the QK waves in period j-3).
     uint32_t stage_bad = 0;   // bit i: the page in latent stage i had an id out of range (wave-uniform)
     auto page_ok = [&](int page) { return page >= 0 && page < a.num_pages; };
     auto copy_latent = [&](int kb, int page) {
@@ -383,26 +381,22 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       for (int i = 0; i < 2; ++i) g2lds16_so(rp + (16 * dq + 8 * i) * (kDr * 2), rope_v, dst + 1024 * (2 * dq + i));
       if (lane < 16) g2lds4_so(sc, sc_off, dst + kRopeBytes + 64 * dq);
     };
-    // prologue: blocks 0 and 1 whole, the latent of block 2
+    // prologue: blocks 0 and 1
     const int pg0 = page_of(0);
     copy_latent(0, pg0);
     copy_rope_scale(0, pg0);
-    int pg_n = 0, pg_nn = 0;                       // page ids of blocks k+2 and k+3 in period k
     if (nblocks > 1) {
       const int pg1 = page_of(1);
       copy_latent(1, pg1);
       copy_rope_scale(1, pg1);
     }
-    if (nblocks > 2) {
-      pg_n = page_of(2);
-      copy_latent(2, pg_n);
-    }
+    int pg_n = nblocks > 2 ? page_of(2) : 0;       // page id of block k+2 in period k
 
     // O[2T + r]: O^T tile of dims 128dq + 32T.. and row tile r
     v16f O[8];
 #pragma unroll
     for (int T = 0; T < 8; ++T) O[T] = v16f{0};
-    bool stored = false, cur_bad = false, defer = false;
+    bool stored = false, cur_bad = false;
 
     // transposed V reads: 16-lane group g16 of half h reads 8 token rows x 16 bytes;
     // lane pair (2i, 2i+1) supplies row i (token of P/V slot 8c + i).  The byte
@@ -416,22 +410,21 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       const int tok = 16 * c + 8 * (tri >> 2) + 4 * h + (tri & 3);
       tr_off[c] = (uint32_t)(tok * kDc + 8 * trb) | (uint32_t)(((8 * dq + g16) ^ swz(tok)) << 4);
     }
-    // Top-of-period wait: block k complete.  Copies issued after its RoPE/scale
-    // part may stay in flight: latent k+1, RoPE/scale k+1 and latent k+2.
+    // Top-of-period wait: block k complete, block k+1 (11 copies) may stay in
+    // flight.  After global stores everything is drained (stores and loads are not
+    // counted in order with each other).
     auto top_barrier = [&](int k) {
       if (stored || k + 1 >= nblocks) barrier_vm_lgkm0<0>();
-      else if (k + 2 >= nblocks) barrier_vm_lgkm0<11>();
-      else barrier_vm_lgkm0<19>();
+      else barrier_vm_lgkm0<11>();
     };
 
     // period 0: no PV product yet
     top_barrier(0);
-    if (nblocks > 2) copy_rope_scale(2, pg_n);
-    if (nblocks > 3) {
-      pg_nn = page_of(3);
-      copy_latent(3, pg_nn);
+    if (nblocks > 2) {
+      copy_latent(2, pg_n);
+      copy_rope_scale(2, pg_n);
+      if (nblocks > 3) pg_n = page_of(3);
     }
-    pg_n = pg_nn;
     enter_piece(gstart);
     cur_bad = (stage_bad & 1u) != 0;
     int prev_valid = min(kPage, cur_n - (gstart - cur_p0) * kPage);   // valid tokens of the pending block
@@ -439,9 +432,11 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     for (int k = 1; k <= nblocks; ++k) {
       top_barrier(k);
       stored = false;
-      if (defer) copy_latent(k + 2, pg_n);         // deferred from the previous period
-      defer = false;
-      if (k + 2 < nblocks) copy_rope_scale(k + 2, pg_n);
+      const bool copy = k + 2 < nblocks;
+      if (copy) {
+        copy_latent(k + 2, pg_n);
+        copy_rope_scale(k + 2, pg_n);
+      }
       // ---- PV of block k-1 with the codes the QK waves published -----------
       const uint32_t st_lds = smem_base + ((k - 1) % kLatStages) * kLatBytes;
       const v4f gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
@@ -454,7 +449,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       // codes and state are in registers: let the QK waves overwrite them
       lds_wait_all();
       if (lane == 0) flag_store(xf + w, k);
-      if (k + 3 < nblocks) pg_nn = page_of(k + 3);   // scalar load, in flight during the product
+      if (k + 3 < nblocks) pg_n = page_of(k + 3);    // scalar load, in flight during the product
       if (prev_valid < kPage) {
         // last page of a sequence: clear the bytes of the slots past its end that
         // this wave reads (stale data could hold NaN codes; their probability
@@ -523,12 +518,6 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
 #pragma unroll
         for (int T = 0; T < 8; ++T) O[T] = v16f{0};
       }
-      // latent of block k+3 (stage of block k-1, whose product is done)
-      if (k + 3 < nblocks) {
-        if (stored) defer = true;
-        else copy_latent(k + 3, pg_nn);
-      }
-      pg_n = pg_nn;
       if (k == nblocks) break;
       // piece bookkeeping for block k (mirrors the QK waves)
       const int gb = gstart + k;
