@@ -3,7 +3,8 @@
 // Each KV piece p of a sequence delivered a normalized partial output o_p and its
 // log-sum-exp LSE_p (Algorithm 1 returns both per query row).  Per row:
 //   LSE = log sum_p exp(LSE_p),   o = sum_p exp(LSE_p - LSE) * o_p.
-// One wave merges one row; lane l owns output dimensions 8l..8l+7.
+// One wave merges one row; lane l owns output dimensions 8l..8l+7.  The pieces'
+// log-sum-exps are read lane-parallel and the partial rows four at a time.
 
 #include "snapmla_device.h"
 #include "snapmla_internal.h"
@@ -46,29 +47,56 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   };
   auto pid = [&](int i) -> int64_t { return balanced ? (int64_t)i + b : (int64_t)b * W + i; };
 
+  // pass 1: lane i reads the log-sum-exp of candidate piece first + i (64 at a
+  // time), the wave reduces the maximum and NaN flag
   float M = -INFINITY;
   bool anynan = false;
-  for (int i = first; i <= last; ++i) {
-    if (!exists(i)) continue;
-    const float x = a.part_lse[pid(i) * a.rows_pad + r];
+  for (int i0 = first; i0 <= last; i0 += 64) {
+    const int i = i0 + lane;
+    float x = -INFINITY;
+    if (i <= last && exists(i)) x = a.part_lse[pid(i) * a.rows_pad + r];
     anynan |= x != x;
     M = fmaxf(M, x);
   }
+  M = wave_max(M);
+  anynan = __builtin_amdgcn_ballot_w64(anynan) != 0;
+  // pass 2: weights exp(LSE_i - M) (lane-parallel), then the weighted rows, four
+  // pieces per round so that their loads overlap
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float S = 0.0f;
   if (M > -INFINITY && !anynan) {
-    for (int i = first; i <= last; ++i) {
-      if (!exists(i)) continue;
-      const int64_t base = pid(i) * a.rows_pad + r;
-      const float x = a.part_lse[base];
-      if (!(x > -INFINITY)) continue;
-      const float wgt = expf(x - M);
-      S += wgt;
-      const v4f* src = reinterpret_cast<const v4f*>(a.part_o + base * kDc + 8 * lane);
-      const v4f u0 = src[0], u1 = src[1];
-      acc[0] += wgt * u0[0]; acc[1] += wgt * u0[1]; acc[2] += wgt * u0[2]; acc[3] += wgt * u0[3];
-      acc[4] += wgt * u1[0]; acc[5] += wgt * u1[1]; acc[6] += wgt * u1[2]; acc[7] += wgt * u1[3];
+    for (int i0 = first; i0 <= last; i0 += 64) {
+      const int i = i0 + lane;
+      float wi = 0.0f;
+      if (i <= last && exists(i)) {
+        const float x = a.part_lse[pid(i) * a.rows_pad + r];
+        wi = x > -INFINITY ? expf(x - M) : 0.0f;
+      }
+      S += wi;
+      const int cnt = min(64, last - i0 + 1);
+      for (int j = 0; j < cnt; j += 4) {
+        v4f u[4][2];
+        float wj[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          wj[t] = __shfl(wi, j + t, 64);              // zero for missing / empty pieces
+          const bool use = j + t < cnt && wj[t] != 0.0f;
+          const int ij = min(i0 + j + t, last);      // in range even when unused
+          const v4f* src = reinterpret_cast<const v4f*>(a.part_o + (pid(ij) * a.rows_pad + r) * kDc + 8 * lane);
+          u[t][0] = use ? src[0] : v4f{0.f, 0.f, 0.f, 0.f};
+          u[t][1] = use ? src[1] : v4f{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          acc[0] += wj[t] * u[t][0][0]; acc[1] += wj[t] * u[t][0][1];
+          acc[2] += wj[t] * u[t][0][2]; acc[3] += wj[t] * u[t][0][3];
+          acc[4] += wj[t] * u[t][1][0]; acc[5] += wj[t] * u[t][1][1];
+          acc[6] += wj[t] * u[t][1][2]; acc[7] += wj[t] * u[t][1][3];
+        }
+      }
     }
+    // wave sum of the weights
+    for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o, 64);
   }
   const bool bad = a.flags[b] != 0 || anynan;
   float o[8];

@@ -396,7 +396,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     v16f O[8];
 #pragma unroll
     for (int T = 0; T < 8; ++T) O[T] = v16f{0};
-    bool stored = false, cur_bad = false;
+    bool cur_bad = false;
 
     // transposed V reads: 16-lane group g16 of half h reads 8 token rows x 16 bytes;
     // lane pair (2i, 2i+1) supplies row i (token of P/V slot 8c + i).  The byte
@@ -411,10 +411,10 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       tr_off[c] = (uint32_t)(tok * kDc + 8 * trb) | (uint32_t)(((8 * dq + g16) ^ swz(tok)) << 4);
     }
     // Top-of-period wait: block k complete, block k+1 (11 copies) may stay in
-    // flight.  After global stores everything is drained (stores and loads are not
-    // counted in order with each other).
+    // flight.  Loads complete in issue order, so "at most 11 outstanding" implies
+    // block k is in LDS even with the previous period's stores still counted.
     auto top_barrier = [&](int k) {
-      if (stored || k + 1 >= nblocks) barrier_vm_lgkm0<0>();
+      if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
       else barrier_vm_lgkm0<11>();
     };
 
@@ -431,7 +431,6 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
 
     for (int k = 1; k <= nblocks; ++k) {
       top_barrier(k);
-      stored = false;
       const bool copy = k + 2 < nblocks;
       if (copy) {
         copy_latent(k + 2, pg_n);
@@ -512,7 +511,6 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
               if (cur_bad) lse = nanv;
               a.part_lse[pid * a.rows_pad + row] = lse;
             }
-            stored = true;
           }
         }
 #pragma unroll
