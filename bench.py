@@ -1,16 +1,23 @@
 """Benchmark of the SnapMLA FP8 MLA decode hot path on one MI355X.
 
 One step = the whole hot path for one batch: quantize-and-append the step's new
-tokens into the paged FP8 cache, quantize the queries, decode every sequence
-(FP8 QK + BF16 RoPE, online softmax, fused/quantized P, FP8 PV), and merge the
-split-KV pieces.  Inputs are resident in HBM before timing starts.
+tokens into the paged FP8 cache (snapmla_quantize_append), quantize the queries
+and decode every sequence (snapmla_decode: FP8 QK + BF16 RoPE, online softmax,
+fused and block-quantized P, FP8 PV), and merge the split-KV pieces
+(snapmla_combine).  Inputs are resident in HBM before timing starts.
 
 Default workload: 64-head MLA decode, batch 64, one query token, ragged context
 lengths uniform in [8192, 32768], 64-token pages in shuffled physical order.
 
-Prints ONE JSON line.  `value` is the achieved KV-cache read rate
-(sum of context lengths x 644 B per token / step time), i.e. the metric's
-"achieved KV HBM GB/s"; `us_per_step` is the step time.
+`value` is the achieved KV-cache read rate, sum of context lengths x 644 B per
+token / step time, over K back-to-back steps.  Also reported: the same step
+captured once as a HIP graph and replayed, cold-cache step times (a 1 GiB
+scratch write and read between steps, outside the timed region: the read
+leaves the caches clean, so no write-back of scratch lines lands inside the
+step), the per-call split, the roofline of the decode call and the CPU oracle
+on a bounded sample.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
 """
 
 import argparse
@@ -29,15 +36,19 @@ BYTES_PER_TOKEN = 512 + 2 * 64 + 4           # e4m3 latent + bf16 rope + f32 sca
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
 
 
+def _log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def _src_hash():
     h = hashlib.sha256()
-    for f in ("decode.hip", "snapmla_device.h"):
+    for f in ("decode.hip", "quant.hip", "snapmla_device.h"):
         h.update(open(os.path.join(ROOT, "paper_2602_10718_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
 def _traffic(workload_name):
-    """HBM bytes per decode launch measured with rocprofv3 counters (profiles/), if still current."""
+    """HBM bytes per decode call measured with rocprofv3 counters (profiles/), if still current."""
     try:
         d = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
@@ -50,7 +61,6 @@ def _traffic(workload_name):
 
 def cpu_baseline(w, budget_s=15.0):
     """The oracle (float64 numpy, as written) on a bounded sample of the same workload."""
-    import numpy as np
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
@@ -74,20 +84,25 @@ def cpu_baseline(w, budget_s=15.0):
         seqs += 1
         if el > budget_s and seqs >= 2:
             break
-    return {"value": toks * BYTES_PER_TOKEN / el / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"{seqs} of {w.B} sequences ({toks} KV tokens, {w.H * w.q_len} rows each), quantize + "
-                      f"decode_streaming; {el:.1f} s; full step extrapolated "
-                      f"{el * w.total_tokens / toks * 1e6:.0f} us"}
+    return {"value": round(toks * BYTES_PER_TOKEN / el / 1e9, 3), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{seqs} of {w.B} sequences ({toks} KV tokens, {w.H * w.q_len} rows each): per-token "
+                      f"quantization + decode_streaming in float64, {el:.1f} s; the full step extrapolates to "
+                      f"{el * w.total_tokens / toks:.1f} s"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=3, help="workload 1..5 (3 is the headline)")
     ap.add_argument("--num-splits", type=int, default=None)
+    ap.add_argument("--cold-steps", type=int, default=20, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="for rocprofv3 --pmc runs: one 256 MiB device copy (counter calibration), then 3 "
+                         "snapmla_decode calls; prints what it ran and exits")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the decode path shards by "
@@ -104,23 +119,51 @@ def main():
     t_fill = time.perf_counter()
     run = DecodeRunner(w, num_splits=args.num_splits, out_dtype=torch.bfloat16)
     t_fill = time.perf_counter() - t_fill
-    print(f"[bench] cache filled ({w.total_tokens} tokens) in {t_fill:.1f} s", file=sys.stderr, flush=True)
+    _log(f"cache filled ({w.total_tokens} tokens) in {t_fill:.1f} s")
     stream = torch.cuda.current_stream()
+    kv_bytes = w.kv_bytes()
 
+    if args.traffic_probe:
+        src = torch.ones(1 << 26, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            run.decode()
+            torch.cuda.synchronize()
+        print(json.dumps({"traffic_probe": True, "copy_bytes_read": src.numel() * 4,
+                          "copy_bytes_written": dst.numel() * 4, "decode_calls": 3, "workload": w.name,
+                          "kv_bytes": kv_bytes}), flush=True)
+        return
+
+    def timed(fn, k):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(k):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / k
+
+    # ---- warm-up, then the timed region: K back-to-back steps ---------------
     for _ in range(args.warmup):
         run.step()
     torch.cuda.synchronize()
+    ms_per_step = timed(run.step, args.steps)
+    _log(f"timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step")
 
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for _ in range(args.steps):
+    # ---- the same step as a HIP graph replay --------------------------------
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
         run.step()
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(end) / args.steps
+    for _ in range(args.warmup):
+        graph.replay()
+    graph_us = timed(graph.replay, args.steps) * 1e3
+    _log(f"graph replay: {graph_us:.1f} us/step")
 
-    # per-call durations over the same number of steps (events on the launch stream)
+    # ---- the same step issued eagerly, with the per-call split ---------------
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for k in range(args.steps):
         ev[k][0].record(stream)
@@ -134,9 +177,29 @@ def main():
     append_us = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
     decode_us = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) * 1e3
     combine_us = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
+    _log(f"per call: append {append_us:.1f} decode {decode_us:.1f} combine {combine_us:.1f} us")
 
-    print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
-    kv_bytes = w.kv_bytes()
+    # ---- cold cache: 1 GiB scratch write + read between steps (not timed) ----
+    cold = None
+    if args.cold_steps > 0:
+        scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        sink = torch.empty((), dtype=torch.float32, device="cuda")
+        ts = []
+        for k in range(args.cold_steps):
+            scratch.fill_(float(k))
+            sink.copy_(scratch.sum())
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            run.step()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        del scratch, sink
+        cold = {"steps": args.cold_steps, "median_us": round(float(np.median(ts)), 1),
+                "p90_us": round(float(np.percentile(ts, 90)), 1),
+                "median_GBps": round(kv_bytes / (float(np.median(ts)) * 1e-6) / 1e9, 1)}
+        _log(f"cold: median {cold['median_us']} us, p90 {cold['p90_us']} us")
+
     gbps = kv_bytes / (ms_per_step * 1e-3) / 1e9
     decode_gbps = kv_bytes / (decode_us * 1e-6) / 1e9
     traffic = _traffic(w.name)
@@ -161,13 +224,15 @@ def main():
             "ctx_min": int(w.seq_lens.min()), "ctx_max": int(w.seq_lens.max()),
             "kv_tokens": w.total_tokens, "kv_bytes": kv_bytes, "page": 64,
             "num_splits": run.num_splits, "kv_chunk_tokens": run.kv_chunk_tokens,
-            "append_per_step": w.n_new,
+            "append_per_step": w.n_new, "step": "append + decode + combine",
         },
+        "us_per_step_graph": round(graph_us, 1),
         "breakdown_us": {"append": round(append_us, 2), "decode": round(decode_us, 2),
                          "combine": round(combine_us, 2)},
+        "cold_cache": cold,
         "roofline": {
             "bound": "hbm",
-            "kernel": "snapmla_decode (query-quantization/plan kernel + decode kernel)",
+            "kernel": "snapmla_decode call (prep_kernel + decode_kernel), HIP events on its stream",
             "achieved": round(decode_gbps, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
@@ -178,6 +243,7 @@ def main():
         "cache_fill_s": round(t_fill, 1),
     }
     if not args.no_cpu_baseline:
+        _log("cpu baseline (oracle) ...")
         line["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(line), flush=True)
 
