@@ -2,37 +2,40 @@
 //
 // One workgroup = 8 waves (two per SIMD) = 64 query rows of one row group x a
 // contiguous range of 64-token KV blocks (one page each).  The waves specialise:
-//   QK waves  w = 0..3, (rt, tt) = (w/2, w%2): S^T tile of row tile rt (32 rows)
-//             and token tile tt (tokens 32tt..32tt+31), online softmax, scale
-//             fusion and E4M3 probability codes; they own q and the row state.
+//   QK waves  w = 0..3: rows 16w..16w+15 against all 64 tokens of a block
+//             (16x16 tiles, tokens on the MFMA M axis, so one lane holds 16
+//             logits of one row and the four lanes of a row complete the block);
+//             online softmax, scale fusion and E4M3 probability codes; they own
+//             q and the row state.
 //   PV waves  w = 4..7, dq = w-4: O^T of all 64 rows for latent dimensions
 //             128dq..128dq+127 (each V^T tile read from LDS once, used for both
-//             row tiles); they own the output accumulator, copy the pages into
-//             LDS and write the partial results.
-// The two QK waves of a row tile exchange tile statistics through LDS with a
-// flag handshake of their own, then publish the probability codes and the
-// per-row state; the PV waves consume them one block later.  So on every SIMD a
-// QK wave works on block k while a PV wave works on block k-1, with one
-// workgroup barrier per block.  The code/state buffers are single: a QK wave
-// overwrites them only after every PV wave has flagged that it holds the
-// previous block's values in registers.  (The paper's Hopper kernel splits the
-// work between two warp groups, Algorithm 1 and Appendix E; here the split is by
-// phase instead of by output half.)
+//             32-row tiles); they own the output accumulator, copy the pages
+//             into LDS and write the piece results.
+// One workgroup barrier opens each period k.  In period k the QK waves turn
+// block k into probability codes and per-row state, publish them in LDS and
+// raise their flags; the PV waves meanwhile run the products of block k-1 (their
+// operands already in registers), issue the copies, take block k's V^T tiles
+// into registers, wait for the QK flags and take block k's codes and state.  So
+// the products of a block run at the top of the next period, the latent stage of
+// block k-1 is free when period k opens, and the code/state buffers are single
+// (the PV waves have read them before the barrier after which the QK waves write
+// them again).  (The paper's Hopper kernel splits the work between two warp
+// groups, Algorithm 1 and Appendix E; here the split is by phase instead of by
+// output half.)
 //
 // Data movement: each 64-token page (32 KiB E4M3 latent, 8 KiB bf16 RoPE,
-// 256 B scales) is copied HBM -> LDS with 16-byte direct-to-LDS loads, two
-// pages ahead of the compute, right after the barrier that opens a period, so
-// every page has two full periods to arrive.  The latent lives four periods in
-// LDS (arriving, arriving, QK, PV) and the RoPE/scale part three (it is only
-// read by the QK waves), hence a 4-stage latent ring and a 3-stage RoPE/scale
-// ring (160 KiB of LDS in all).  Latent rows are stored with the 16-byte chunk
-// index XOR-swizzled by the token index (swz) so that both the token-major QK
-// reads and the transposed PV reads avoid bank conflicts.  Page ids are read
-// with scalar loads one block ahead of their copy.
+// 256 B scales) is copied HBM -> LDS with 16-byte direct-to-LDS loads right
+// after the barrier that opens a period: the latent three blocks ahead of the QK
+// waves, the RoPE/scale part two.  The latent lives four periods in LDS (three
+// arriving, one in use) and the RoPE/scale part three, hence a 4-stage latent
+// ring and a 3-stage RoPE/scale ring (160 KiB of LDS in all).  Latent rows are
+// stored with the 16-byte chunk index XOR-swizzled by the token index (swz) so
+// that both the token-major QK reads and the transposed PV reads avoid bank
+// conflicts.  Page ids travel the same way, four blocks ahead of their copy.
 //
 // Per block (matrices transposed so that one lane owns one query row):
-//   S^T[32 tok x 32 rows]  = K_c^T . q8^T   (32x32x64 FP8 MFMA, K = 512)
-//                          + K_r^T . q_r^T  (32x32x16 BF16 MFMA, K = 64)
+//   S^T[16 tok x 16 rows]  = K_c^T . q8^T   (16x16x128 FP8 MFMA, K = 512), 4 token tiles
+//                          + K_r^T . q_r^T  (16x16x32 BF16 MFMA, K = 64)
 //   s = log2(e) tau (sigma_q sigma_K acc_c + acc_r)   (Section 3.1 domain alignment,
 //       applied to the two accumulators instead of pre-scaling the RoPE operands)
 //   running max m, block scale sigma_P = max(max(e sigma_K) / 448, 2^-40),
@@ -41,8 +44,10 @@
 //   O^T[128 dims x 64 rows] = gamma O^T + V^T . P^T       (FP8 MFMA, K = 64 tokens)
 // V^T is read straight from the token-major latent tile with the LDS transpose
 // read (ds_read_b64_tr_b8; the CDNA counterpart of the paper's V-tile
-// transposition) and the P codes are already in the B-operand layout, so no
-// accumulator permutation is needed.  Blocks are consumed in increasing order,
+// transposition).  The K (token) order of the PV product is chosen so that each
+// QK lane's 16 codes are one contiguous 16-byte piece of a PV lane's B operand,
+// and the transposed reads fetch V rows in that same order: no accumulator
+// permutation is needed.  Blocks are consumed in increasing order,
 // the monotone order of Appendix E.  Slots past the end of a sequence hold
 // stale bytes; their logits are masked to -inf, their fused probabilities
 // forced to 0 and their V bytes cleared before the PV product.
@@ -61,11 +66,12 @@ constexpr int kRsStages = 3;
 constexpr int kRsBase = kLatStages * kLatBytes;   // LDS offset of the RoPE/scale ring
 constexpr int kXBase = kRsBase + kRsStages * kRsBytes;
 constexpr int kWaves = 8;
-constexpr int kXsBytes = 2 * 2 * 32 * 16;       // tile statistics [rt][tt][row] x float4
-constexpr int kXcBytes = 2 * 2 * 64 * 16;       // probability codes [rt][tt][lane] x 16 B
+constexpr int kXcBytes = 64 * 64;               // probability codes [row][64 token slots]
 constexpr int kXgBytes = 2 * 32 * 16;           // per-row gamma, l, m, sigma_p [rt][row] x float4
-constexpr int kXfBytes = 8 * 4;                 // handshake flags: [QK wave], [PV wave]
-constexpr int kSmemBytes = kXBase + kXsBytes + kXcBytes + kXgBytes + kXfBytes;
+constexpr int kXfBytes = 4 * 4;                 // handshake flags of the QK waves
+constexpr int kXpBytes = 4 * 4 * 4;             // page-id ring of the PV waves [wave][4 slots]
+constexpr int kXpBase = kXBase + kXcBytes + kXgBytes + kXfBytes;
+constexpr int kSmemBytes = kXpBase + kXpBytes;
 static_assert(kSmemBytes <= 160 * 1024, "LDS budget of one workgroup");
 constexpr float kLn2 = 0.69314718055994531f;
 // Upper bound on the polls of a handshake wait.  The waits end by construction
@@ -73,11 +79,13 @@ constexpr float kLn2 = 0.69314718055994531f;
 // anything); the bound only guarantees that the kernel terminates.
 constexpr int kSpinLimit = 1 << 22;
 
-// Latent rows are stored with 16-byte chunk c of token t at chunk c ^ swz(t).
-// Eight consecutive tokens (token-major QK reads) and the eight tokens
-// {t0..t0+3, t0+8..t0+11} of one transposed-read group (PV reads) both map a
-// given chunk to eight distinct 128-byte bank lines.
-__device__ __forceinline__ int swz(int t) { return (t & 31) ^ (((t >> 3) & 1) << 2); }
+// Latent rows are stored with 16-byte chunk c of token t at chunk c ^ swz(t),
+// RoPE rows with chunk c at c ^ rswz(t).  Sixteen consecutive tokens (the QK
+// operand reads) map a given chunk to sixteen distinct 16-byte bank groups, and
+// the eight tokens of one transposed-read group (PV reads: t0..t0+3 and
+// t0+16..t0+19) to eight distinct groups of a 128-byte line.
+__device__ __forceinline__ int swz(int t) { return (t & 15) ^ (((t >> 4) & 1) << 2); }
+__device__ __forceinline__ int rswz(int t) { return (t >> 1) & 7; }
 
 // Largest b with prefix[b] <= gb (prefix is non-decreasing, prefix[B] > gb).
 __device__ __forceinline__ int find_seq(const int32_t* __restrict__ prefix, int B, int gb) {
@@ -107,10 +115,9 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
                                                         const int32_t* __restrict__ page_table,
                                                         const int32_t* __restrict__ seq_lens) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmemBytes];
-  float* xs = reinterpret_cast<float*>(smem + kXBase);                          // [rt][tt][32] x 4
-  v4i* xc = reinterpret_cast<v4i*>(smem + kXBase + kXsBytes);                   // [rt][tt][64]
-  float* xg = reinterpret_cast<float*>(smem + kXBase + kXsBytes + kXcBytes);    // [64 rows] x 4
-  int* xf = reinterpret_cast<int*>(smem + kXBase + kXsBytes + kXcBytes + kXgBytes);   // [0..3] QK, [4..7] PV
+  uint8_t* xc = smem + kXBase;                                                 // [64 rows][64] codes
+  float* xg = reinterpret_cast<float*>(smem + kXBase + kXcBytes);               // [64 rows] x 4
+  int* xf = reinterpret_cast<int*>(smem + kXBase + kXcBytes + kXgBytes);        // QK flags
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -154,32 +161,35 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     cur_n = seq_lens[b];
   };
 
-  if (lane == 0) flag_store(xf + w, 0);            // ordered before any wait by the first barrier
+  if (is_qk && lane == 0) flag_store(xf + w, 0);   // ordered before any wait by the first barrier
 
   if (is_qk) {
     // ======================= QK / softmax waves ==============================
-    const int rt = w >> 1, half = w & 1;           // half = token tile
-    const int row = 64 * g + 32 * rt + n;          // query row of this lane within the sequence
+    // lane (n16, g4): row 16w + n16; its 16 logits per block are the tokens
+    // 16t + 4g4 + v of the four 16-token tiles t (v = 0..3)
+    const int n16 = lane & 15, g4 = lane >> 4;
+    const int row = 64 * g + 16 * w + n16;         // query row of this lane within the sequence
     const bool row_ok = row < a.R;
     const float sl2 = a.sl2;
     float cq = 0.f;                 // sigma_q
-    v8i qv[8];
-    v4i qr[4];
+    v8i qv[4];                      // q8 bytes 128s + 32g4 .. +31 (B operand of K-step s)
+    v4i qr[2];                      // q_rope elements 32s + 8g4 .. +7
     float m = -INFINITY, sp = 1.0f, l = 0.0f;
     int vis = 0;
-    // per-lane LDS byte offsets inside a stage (constant across blocks): the 16
-    // latent chunks of this lane's token for the 8 K-steps, its 4 RoPE chunks and
-    // the scales of its 16 tokens (4 x float4)
-    uint32_t koff[16], roff[4], soff[4];
+    // per-lane LDS byte offsets inside a stage (constant across blocks):
+    //   latent chunk of K-step s, half c of token tile t:
+    //     8192 t + (koff[t & 1][c] ^ 128 s)       (swz folded in)
+    //   RoPE chunk of step s of tile t:  2048 t + roff[s];  scales: 64 t + soff
+    uint32_t koff[2][2], roff[2];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      koff[2 * s] = (32 * half + n) * kDc + (((4 * s + 2 * h) ^ swz(n)) << 4);
-      koff[2 * s + 1] = (32 * half + n) * kDc + (((4 * s + 2 * h + 1) ^ swz(n)) << 4);
+    for (int par = 0; par < 2; ++par) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        koff[par][c] = (uint32_t)((n16 * kDc + (((2 * g4 + c) ^ (n16 & 7) ^ (4 * par)) << 4)) | (128 * (n16 >> 3)));
     }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) roff[s] = (32 * half + n) * (kDr * 2) + (((2 * s + h) ^ (n & 7)) << 4);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) soff[q] = kRopeBytes + 4 * (32 * half + 8 * q + 4 * h);
+    for (int s = 0; s < 2; ++s) roff[s] = (uint32_t)(n16 * (kDr * 2) + (((4 * s + g4) ^ (n16 >> 1)) << 4));
+    const uint32_t soff = (uint32_t)(kRopeBytes + 16 * g4);
 
     for (int k = 0; k < nblocks; ++k) {
       barrier_vm_lgkm0<63>();                              // page k has landed (PV waves waited)
@@ -191,19 +201,19 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           const int64_t qrow = (int64_t)cur_b * a.R + row;
           const v4i* src = reinterpret_cast<const v4i*>(a.q8 + qrow * kDc);
 #pragma unroll
-          for (int s = 0; s < 8; ++s) {
-            const v4i lo4 = src[4 * s + 2 * h], hi4 = src[4 * s + 2 * h + 1];
+          for (int s = 0; s < 4; ++s) {
+            const v4i lo4 = src[8 * s + 2 * g4], hi4 = src[8 * s + 2 * g4 + 1];
             qv[s] = v8i{lo4[0], lo4[1], lo4[2], lo4[3], hi4[0], hi4[1], hi4[2], hi4[3]};
           }
           const v4i* rsrc = reinterpret_cast<const v4i*>(a.q_rope + qrow * kDr);
 #pragma unroll
-          for (int s = 0; s < 4; ++s) qr[s] = rsrc[2 * s + h];
+          for (int s = 0; s < 2; ++s) qr[s] = rsrc[4 * s + g4];
           cq = a.sq[qrow];
         } else {
 #pragma unroll
-          for (int s = 0; s < 8; ++s) qv[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0};
+          for (int s = 0; s < 4; ++s) qv[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-          for (int s = 0; s < 4; ++s) qr[s] = v4i{0, 0, 0, 0};
+          for (int s = 0; s < 2; ++s) qr[s] = v4i{0, 0, 0, 0};
           cq = 0.f;
         }
         m = -INFINITY; sp = 1.0f; l = 0.0f;
@@ -212,115 +222,107 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       const uint8_t* st = smem + (k % kLatStages) * kLatBytes;             // latent of block k
       const uint8_t* sr = smem + kRsBase + (k % kRsStages) * kRsBytes;     // its RoPE and scales
 
-      // ---- S^T tile = K . Q^T: every operand of the block is requested before the
-      // first product, so the LDS latency is paid once per block
+      // ---- S^T tiles = K . Q^T, token tile by token tile; the operands of tiles
+      // t+1 (and t+2) are requested before the products of tile t
       v4f skq[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) skq[q] = *reinterpret_cast<const v4f*>(sr + soff[q]);
-      v4i kc[16], kr[4];
+      for (int t = 0; t < 4; ++t) skq[t] = *reinterpret_cast<const v4f*>(sr + soff + 64 * t);
+      v4f accC[4], accR[4];
+      v4i kc[2][4][2], kr[2][2];
+      auto load_tile = [&](int t, int slot) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) kc[i] = *reinterpret_cast<const v4i*>(st + koff[i]);
+        for (int s = 0; s < 4; ++s) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kr[i] = *reinterpret_cast<const v4i*>(sr + roff[i]);
-      __builtin_amdgcn_sched_barrier(0);           // keep the reads ahead of the products
-      v16f accC = v16f{0}, accR = v16f{0};
+          for (int c = 0; c < 2; ++c)
+            kc[slot][s][c] = *reinterpret_cast<const v4i*>(st + 8192 * t + (koff[t & 1][c] ^ (uint32_t)(128 * s)));
+        }
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        accC = mfma_f8_32x32x64(v8i{kc[2 * s][0], kc[2 * s][1], kc[2 * s][2], kc[2 * s][3], kc[2 * s + 1][0],
-                                    kc[2 * s + 1][1], kc[2 * s + 1][2], kc[2 * s + 1][3]},
-                                qv[s], accC);
-        if (s < 4) accR = mfma_bf16_32x32x16(kr[s], qr[s], accR);
+        for (int s = 0; s < 2; ++s) kr[slot][s] = *reinterpret_cast<const v4i*>(sr + 2048 * t + roff[s]);
+      };
+      load_tile(0, 0);
+      load_tile(1, 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int slot = t & 1;
+        v4f c4 = v4f{0.f, 0.f, 0.f, 0.f}, r4 = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          c4 = mfma_f8_16x16x128(v8i{kc[slot][s][0][0], kc[slot][s][0][1], kc[slot][s][0][2], kc[slot][s][0][3],
+                                     kc[slot][s][1][0], kc[slot][s][1][1], kc[slot][s][1][2], kc[slot][s][1][3]},
+                                 qv[s], c4);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) r4 = mfma_bf16_16x16x32(kr[slot][s], qr[s], r4);
+        accC[t] = c4;
+        accR[t] = r4;
+        if (t + 2 < 4) load_tile(t + 2, slot);
+        __builtin_amdgcn_sched_barrier(0);
       }
 
-      // ---- tile statistics: lane (row n, half h) holds tokens 32tt + 8(v/4) + 4h + v%4
+      // ---- block statistics of this row (16 logits here, 48 in lanes n16 + 16 g')
       float sk[16], pp[16];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        sk[4 * q + 0] = skq[q][0]; sk[4 * q + 1] = skq[q][1]; sk[4 * q + 2] = skq[q][2]; sk[4 * q + 3] = skq[q][3];
-      }
-      // raw logits u = sigma_q sigma_K acc_c + acc_r; s = tau log2(e) u enters the
-      // exponentials through one fma each
+      for (int t = 0; t < 4; ++t) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) pp[v] = fmaf(accC[v], cq * sk[v], accR[v]);
+        for (int v = 0; v < 4; ++v) {
+          sk[4 * t + v] = skq[t][v];
+          // raw logit u = sigma_q sigma_K acc_c + acc_r; s = tau log2(e) u enters the
+          // exponentials through one fma each
+          pp[4 * t + v] = fmaf(accC[t][v], cq * skq[t][v], accR[t][v]);
+        }
+      }
       const bool tail = (blk + 1) * kPage > vis;   // some token of this block is hidden from this row
       if (tail) {
-        // hidden tokens and stale slots past the sequence end: logit -inf
+        // hidden tokens and stale slots past the sequence end: logit -inf, scale 0
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int j = blk * kPage + 32 * half + 8 * (v >> 2) + 4 * h + (v & 3);
-          pp[v] = j < vis ? pp[v] : -INFINITY;
+        for (int i = 0; i < 16; ++i) {
+          const int j = blk * kPage + 16 * (i >> 2) + 4 * g4 + (i & 3);
+          const bool vis_j = j < vis;
+          pp[i] = vis_j ? pp[i] : -INFINITY;
+          sk[i] = vis_j ? sk[i] : 0.0f;
         }
       }
       float mt = fmaxf(fmaxf(fmaxf(pp[0], pp[1]), fmaxf(pp[2], pp[3])), fmaxf(fmaxf(pp[4], pp[5]), fmaxf(pp[6], pp[7])));
       mt = fmaxf(mt, fmaxf(fmaxf(fmaxf(pp[8], pp[9]), fmaxf(pp[10], pp[11])),
                            fmaxf(fmaxf(pp[12], pp[13]), fmaxf(pp[14], pp[15]))));
-      mt = xhalf_max(mt) * sl2;                    // tile max of this row (log2 units)
-      float mloc = fmaxf(m, mt);                   // reference of this tile's exponentials
-      mloc = mloc > -INFINITY ? mloc : 0.0f;       // all -inf: exponentials become 0
-      float e[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(fmaf(pp[v], sl2, -mloc));
-      if (tail) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sk[v] = pp[v] > -INFINITY ? sk[v] : 0.0f;   // stale scales may be NaN
-      }
-#pragma unroll
-      for (int v = 0; v < 16; ++v) pp[v] = e[v] * sk[v];
-      float esum = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
-      esum += ((e[8] + e[9]) + (e[10] + e[11])) + ((e[12] + e[13]) + (e[14] + e[15]));
-      float pmax = fmaxf(fmaxf(fmaxf(pp[0], pp[1]), fmaxf(pp[2], pp[3])), fmaxf(fmaxf(pp[4], pp[5]), fmaxf(pp[6], pp[7])));
-      pmax = fmaxf(pmax, fmaxf(fmaxf(fmaxf(pp[8], pp[9]), fmaxf(pp[10], pp[11])),
-                               fmaxf(fmaxf(pp[12], pp[13]), fmaxf(pp[14], pp[15]))));
-      esum = xhalf_sum(esum);
-      pmax = xhalf_max(pmax);
-      if (h == 0) *reinterpret_cast<v4f*>(xs + ((rt * 2 + half) * 32 + n) * 4) = v4f{mt, esum, pmax, 0.f};
-      // handshake with the other QK wave of this row tile: publish, then wait
-      // for its statistics of the same block (it never waits on anything else
-      // before publishing, so the wait ends)
-      lds_wait_all();
-      if (lane == 0) flag_store(xf + w, k + 1);
-      for (int spin = 0; spin < kSpinLimit && flag_load(xf + (w ^ 1)) != k + 1; ++spin) {
-      }
-      asm volatile("" ::: "memory");
-
-      // ---- block statistics, state update, probability codes --------------
-      const v4f s0 = *reinterpret_cast<const v4f*>(xs + ((rt * 2 + 0) * 32 + n) * 4);
-      const v4f s1 = *reinterpret_cast<const v4f*>(xs + ((rt * 2 + 1) * 32 + n) * 4);
-      const float mb = fmaxf(s0[0], s1[0]);         // block max of the raw logits
+      const float mb = quad_max(mt) * sl2;         // block max of this row (log2 units)
       v4i mine = v4i{0, 0, 0, 0};
       float gam = 1.0f;
-      if (mb > -INFINITY) {                         // the row sees a token of this block
+      if (mb > -INFINITY) {                        // the row sees a token of this block
         const float m_new = fmaxf(m, mb);
-        const float a0 = __builtin_amdgcn_exp2f(fmaxf(m, s0[0]) - m_new);
-        const float a1 = __builtin_amdgcn_exp2f(fmaxf(m, s1[0]) - m_new);
-        const float lsum = a0 * s0[1] + a1 * s1[1];
-        const float pbmax = fmaxf(a0 * s0[2], a1 * s1[2]);
+        float e[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) e[i] = __builtin_amdgcn_exp2f(fmaf(pp[i], sl2, -m_new));
+#pragma unroll
+        for (int i = 0; i < 16; ++i) pp[i] = e[i] * sk[i];
+        float esum = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+        esum += ((e[8] + e[9]) + (e[10] + e[11])) + ((e[12] + e[13]) + (e[14] + e[15]));
+        float pmax = fmaxf(fmaxf(fmaxf(pp[0], pp[1]), fmaxf(pp[2], pp[3])), fmaxf(fmaxf(pp[4], pp[5]), fmaxf(pp[6], pp[7])));
+        pmax = fmaxf(pmax, fmaxf(fmaxf(fmaxf(pp[8], pp[9]), fmaxf(pp[10], pp[11])),
+                                 fmaxf(fmaxf(pp[12], pp[13]), fmaxf(pp[14], pp[15]))));
+        esum = quad_sum(esum);
+        pmax = quad_max(pmax);
         // (reciprocals instead of divisions: off by at most an ulp, far inside the
         // rounding slack of the probability codes)
-        const float sP = fmaxf(pbmax * (1.0f / kFp8Max), kEps);
+        const float sP = fmaxf(pmax * (1.0f / kFp8Max), kEps);
         const float inv = __builtin_amdgcn_rcpf(sP);
         gam = __builtin_amdgcn_exp2f(m - m_new) * (sp * inv);
-        l = gam * l + lsum * inv;
+        l = gam * l + esum * inv;
         m = m_new;
         sp = sP;
-        const float f = (half == 0 ? a0 : a1) * inv;
 #pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          int wd = cvt_pk_e4m3(pp[4 * d + 0] * f, pp[4 * d + 1] * f, 0, false);
-          wd = cvt_pk_e4m3(pp[4 * d + 2] * f, pp[4 * d + 3] * f, wd, true);
-          mine[d] = wd;
+        for (int t = 0; t < 4; ++t) {
+          int wd = cvt_pk_e4m3(pp[4 * t + 0] * inv, pp[4 * t + 1] * inv, 0, false);
+          wd = cvt_pk_e4m3(pp[4 * t + 2] * inv, pp[4 * t + 3] * inv, wd, true);
+          mine[t] = wd;
         }
       }
-      // the PV waves hold block k-1's codes and state once all four flagged k
-      if (k > 0) {
-        for (int spin = 0; spin < kSpinLimit; ++spin) {
-          const v4i f4 = flag_load4(xf + 4);
-          if (f4[0] >= k && f4[1] >= k && f4[2] >= k && f4[3] >= k) break;
-        }
-        asm volatile("" ::: "memory");
-      }
-      xc[(rt * 2 + half) * 64 + lane] = mine;
-      if (half == 0 && h == 0) *reinterpret_cast<v4f*>(xg + (32 * rt + n) * 4) = v4f{gam, l, m, sp};
+      // codes of tokens 16t + 4g4 + v at byte 16 g4 + 4t + v of the row; the PV
+      // waves read the previous block's before this period's barrier
+      *reinterpret_cast<v4i*>(xc + (16 * w + n16) * 64 + 16 * g4) = mine;
+      if (g4 == 0) *reinterpret_cast<v4f*>(xg + (16 * w + n16) * 4) = v4f{gam, l, m, sp};
+      lds_wait_all();
+      if (lane == 0) flag_store(xf + w, k + 1);   // block k published
     }
     barrier_vm_lgkm0<63>();                        // pairs with the PV waves' last top barrier
   } else {
@@ -330,27 +332,44 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     // This wave copies latent rows 16dq..16dq+15 (instruction j: rows 16dq + 2j + h,
     // LDS chunk n of the row takes global chunk n ^ swz(row)), RoPE rows
     // 16dq..16dq+15 and scales 16dq..16dq+15 of each page.  For row t = 16dq + 2j + h,
-    // n ^ swz(t) = (n ^ h) ^ cj with the wave-uniform cj = (16(dq&1) + 2j) ^ (j >= 4 ? 4 : 0),
-    // so one per-lane register serves all eight latent copies:
+    // n ^ swz(t) = (n ^ h) ^ cj with the wave-uniform cj = 2j ^ 4(dq & 1), so one
+    // per-lane register serves all eight latent copies:
     //   global offset = (16dq + 2j) * 512 + (lat_v ^ (cj << 4)).
     const uint32_t lat_v = (uint32_t)((((n ^ h) << 4)) | (h << 9));
-    // RoPE instruction j covers rows 16dq + 8j + lane/8, chunk lane%8 ^ (lane/8)
-    const uint32_t rope_v = (uint32_t)((lane >> 3) * (kDr * 2) + (((lane & 7) ^ (lane >> 3)) << 4));
+    // RoPE instruction j covers rows 16dq + 8j + lane/8; LDS chunk lane%8 takes global
+    // chunk (lane%8) ^ rswz(row) = (lane%8) ^ ((lane/16) & 3) ^ 4j:
+    //   global offset = (16dq + 8j) * 128 + (rope_v ^ (j << 6)).
+    const uint32_t rope_v = (uint32_t)((lane >> 3) * (kDr * 2) + (((lane & 7) ^ ((lane >> 4) & 3)) << 4));
     const uint32_t sc_off = (uint32_t)((16 * dq + (lane & 15)) * 4);
     const uint32_t smem_base = lds_offset(smem);
 
-    // issue cursor (scalar): the next block to copy lies in sequence ib, whose
-    // blocks are global blocks [ib_lo, ib_hi).  Blocks are requested in order.
+    // page-table cursor (scalar): the next block asked for lies in sequence ib,
+    // whose blocks are global blocks [ib_lo, ib_hi).  Blocks are asked for in
+    // nondecreasing order; past the range the last block stands in.
     int ib = find_seq(prefix, a.B, gstart);
     int ib_lo = prefix[ib], ib_hi = prefix[ib + 1];
-    auto page_of = [&](int kb) -> int {
-      const int gb = gstart + kb;
+    auto page_entry = [&](int kb) -> const int32_t* {
+      const int gb = gstart + min(kb, nblocks - 1);
       while (gb >= ib_hi) {                        // skips sequences without blocks
         ++ib;
         ib_lo = ib_hi;
         ib_hi = prefix[ib + 1];
       }
-      return page_table[(int64_t)ib * a.max_pages + (gb - ib_lo)];
+      return page_table + (int64_t)ib * a.max_pages + (gb - ib_lo);
+    };
+    // In the loop, page ids come through the copy path rather than the scalar
+    // cache: a scalar load shares its wait counter with the LDS reads, so every
+    // LDS wait of the period would also wait for it, a full memory round trip
+    // under the copy traffic.  In each copying period k every PV wave requests
+    // (one lane, one dword) the id of block k+6 into slot (k+6) % 4 of its ring;
+    // the request is complete at the top of period k+2, at whose end the slot is
+    // read (the id of the latent copy of period k+3).  A slot is read before it
+    // is requested again.
+    const uint32_t pg_ring = smem_base + kXpBase + 16 * dq;
+    const int* pg_ring_p = reinterpret_cast<const int*>(smem + kXpBase + 16 * dq);
+    auto request_page = [&](int kb) {
+      const int32_t* e = page_entry(kb);            // cursor update in uniform control flow
+      if (lane == 0) g2lds4_so(reinterpret_cast<const uint8_t*>(e), 0u, pg_ring + 4 * (kb & 3));
     };
     // Copies per PV wave and page: 8 latent instructions, then 2 RoPE + 1 scale
     // instruction, addressed by a wave-uniform base and the per-lane offsets above.
@@ -368,7 +387,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       const uint32_t dst = smem_base + stg * kLatBytes;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const uint32_t cj = (uint32_t)(((16 * (dq & 1) + 2 * i) ^ (i >= 4 ? 4 : 0)) << 4);
+        const uint32_t cj = (uint32_t)(((2 * i) ^ (4 * (dq & 1))) << 4);
         g2lds16_so(src + (16 * dq + 2 * i) * kDc, lat_v ^ cj, dst + 1024 * (8 * dq + i));
       }
     };
@@ -378,153 +397,173 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       const uint8_t* sc = reinterpret_cast<const uint8_t*>(a.kv_scale) + (int64_t)page * kScBytes;
       const uint32_t dst = smem_base + kRsBase + (kb % kRsStages) * kRsBytes;
 #pragma unroll
-      for (int i = 0; i < 2; ++i) g2lds16_so(rp + (16 * dq + 8 * i) * (kDr * 2), rope_v, dst + 1024 * (2 * dq + i));
+      for (int i = 0; i < 2; ++i)
+        g2lds16_so(rp + (16 * dq + 8 * i) * (kDr * 2), rope_v ^ (uint32_t)(i << 6), dst + 1024 * (2 * dq + i));
       if (lane < 16) g2lds4_so(sc, sc_off, dst + kRopeBytes + 64 * dq);
     };
-    // prologue: blocks 0 and 1
-    const int pg0 = page_of(0);
-    copy_latent(0, pg0);
-    copy_rope_scale(0, pg0);
-    if (nblocks > 1) {
-      const int pg1 = page_of(1);
+    // Copy requests, in issue order.  Prologue: page ids 4 and 5, latent+RoPE of
+    // blocks 0 and 1, latent of block 2.  Period k (while k + 2 < nblocks): page
+    // id k+6, RoPE of block k+2, latent of block k+3: 1 + 3 + 8 = 12 requests.
+    // Requests for blocks past the range repeat the last block's page into the
+    // stage that block would take, which nothing reads afterwards.
+    // (the cursor only moves forward: blocks are asked for in increasing order)
+    int pg_rope, pg_lat;                           // ids of the RoPE and latent copies of the period
+    {
+      const int pg0 = *page_entry(0);
+      const int pg1 = *page_entry(1);
+      pg_rope = *page_entry(2);
+      pg_lat = *page_entry(3);
+      request_page(4);
+      request_page(5);
+      copy_latent(0, pg0);
+      copy_rope_scale(0, pg0);
       copy_latent(1, pg1);
       copy_rope_scale(1, pg1);
+      copy_latent(2, pg_rope);
     }
-    int pg_n = nblocks > 2 ? page_of(2) : 0;       // page id of block k+2 in period k
 
     // O[2T + r]: O^T tile of dims 128dq + 32T.. and row tile r
     v16f O[8];
 #pragma unroll
     for (int T = 0; T < 8; ++T) O[T] = v16f{0};
-    bool cur_bad = false;
 
     // transposed V reads: 16-lane group g16 of half h reads 8 token rows x 16 bytes;
-    // lane pair (2i, 2i+1) supplies row i (token of P/V slot 8c + i).  The byte
-    // offset of tile T, read c inside a stage is tr_off[c] ^ (T << 5): the row
-    // offset, byte half and swizzled chunk ((8dq + g16) ^ swz(tok)) ^ 2T occupy
-    // disjoint bits, and so does the stage base.
+    // lane pair (2i, 2i+1) supplies row i.  K index 32h + 8c + i of the PV product
+    // is token 32(c&1) + 16(i>>2) + 8h + 4(c>>1) + (i&3): the token whose code the
+    // QK waves store at byte 32h + 8c + i of the row.  The byte offset of tile T,
+    // read c inside a stage is tr_off[c] ^ (T << 5): the row offset, byte half and
+    // swizzled chunk ((8dq + g16) ^ swz(tok)) ^ 2T occupy disjoint bits, and so
+    // does the stage base.
     const int q16 = lane & 15, tri = q16 >> 1, trb = q16 & 1, g16 = (lane >> 4) & 1;
     uint32_t tr_off[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int tok = 16 * c + 8 * (tri >> 2) + 4 * h + (tri & 3);
+      const int tok = 32 * (c & 1) + 16 * (tri >> 2) + 8 * h + 4 * (c >> 1) + (tri & 3);
       tr_off[c] = (uint32_t)(tok * kDc + 8 * trb) | (uint32_t)(((8 * dq + g16) ^ swz(tok)) << 4);
     }
-    // Top-of-period wait: block k complete, block k+1 (11 copies) may stay in
-    // flight.  Loads complete in issue order, so "at most 11 outstanding" implies
-    // block k is in LDS even with the previous period's stores still counted.
+    // Top-of-period wait: block k (latent and RoPE) complete, and the page id
+    // read at the end of the period.  Loads complete in issue order: in steady
+    // state the RoPE copy of block k is followed by the latent copy of block k+1
+    // and the 12 requests of period k-1, so "at most 20 outstanding" suffices
+    // (19 in period 0, after the prologue); the period's stores, issued after its
+    // copies, only make the wait stricter.
     auto top_barrier = [&](int k) {
       if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
-      else barrier_vm_lgkm0<11>();
+      else if (k == 0) barrier_vm_lgkm0<19>();
+      else barrier_vm_lgkm0<20>();
     };
 
-    // period 0: no PV product yet
-    top_barrier(0);
-    if (nblocks > 2) {
-      copy_latent(2, pg_n);
-      copy_rope_scale(2, pg_n);
-      if (nblocks > 3) pg_n = page_of(3);
-    }
-    enter_piece(gstart);
-    cur_bad = (stage_bad & 1u) != 0;
-    int prev_valid = min(kPage, cur_n - (gstart - cur_p0) * kPage);   // valid tokens of the pending block
-
-    for (int k = 1; k <= nblocks; ++k) {
+    v2i rv[4][4];                 // V^T tiles of the pending block
+    v8i P0, P1;                   // its codes, row tiles 0 and 1
+    v4f gl0, gl1;                 // its per-row state {gamma, l, m, sigma_P}
+    bool cur_bad = false;
+    for (int k = 0;; ++k) {
       top_barrier(k);
-      const bool copy = k + 2 < nblocks;
-      if (copy) {
-        copy_latent(k + 2, pg_n);
-        copy_rope_scale(k + 2, pg_n);
+      if (k + 2 < nblocks) {
+        request_page(k + 6);
+        copy_rope_scale(k + 2, pg_rope);
+        copy_latent(k + 3, pg_lat);
+        pg_rope = pg_lat;
       }
-      // ---- PV of block k-1 with the codes the QK waves published -----------
-      const uint32_t st_lds = smem_base + ((k - 1) % kLatStages) * kLatBytes;
-      const v4f gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
-      const v4f gl1 = *reinterpret_cast<const v4f*>(xg + (n + 32) * 4);
-      const v4i c00 = xc[0 * 64 + lane], c01 = xc[1 * 64 + lane];
-      const v4i c10 = xc[2 * 64 + lane], c11 = xc[3 * 64 + lane];
-      const v8i P0 = v8i{c00[0], c00[1], c00[2], c00[3], c01[0], c01[1], c01[2], c01[3]};
-      const v8i P1 = v8i{c10[0], c10[1], c10[2], c10[3], c11[0], c11[1], c11[2], c11[3]};
-      const float gam0 = gl0[0], gam1 = gl1[0];
-      // codes and state are in registers: let the QK waves overwrite them
-      lds_wait_all();
-      if (lane == 0) flag_store(xf + w, k);
-      if (k + 3 < nblocks) pg_n = page_of(k + 3);    // scalar load, in flight during the product
-      if (prev_valid < kPage) {
-        // last page of a sequence: clear the bytes of the slots past its end that
-        // this wave reads (stale data could hold NaN codes; their probability
-        // codes are 0)
-        uint8_t* stp = smem + ((k - 1) % kLatStages) * kLatBytes;
-        const int nz = (kPage - prev_valid) * 8;
-        for (int i = lane; i < nz; i += 64) {
-          const int t = prev_valid + (i >> 3);
-          const int c = 8 * dq + (i & 7);
-          *reinterpret_cast<v4i*>(stp + t * kDc + ((c ^ swz(t)) << 4)) = v4i{0, 0, 0, 0};
+      if (k > 0) {
+        // ---- PV of block k-1 --------------------------------------------------
+#pragma unroll
+        for (int T = 0; T < 4; ++T) {
+          O[2 * T] *= gl0[0];
+          O[2 * T + 1] *= gl1[0];
         }
-      }
-      // all 16 transposed reads first, then the rescale, then the 8 products
-      v2i rv[4][4];
 #pragma unroll
-      for (int T = 0; T < 4; ++T) {
+        for (int T = 0; T < 4; ++T) {
+          const v8i A = v8i{rv[T][0][0], rv[T][0][1], rv[T][1][0], rv[T][1][1],
+                            rv[T][2][0], rv[T][2][1], rv[T][3][0], rv[T][3][1]};
+          O[2 * T] = mfma_f8_32x32x64(A, P0, O[2 * T]);
+          O[2 * T + 1] = mfma_f8_32x32x64(A, P1, O[2 * T + 1]);
+        }
+        // ---- end of a piece: write the normalized partial output and LSE ----
+        // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
+        if (k == nblocks || gstart + k >= cur_end) {
+          const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
+                                                  : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
+          const float nanv = __builtin_nanf("");
 #pragma unroll
-        for (int c = 0; c < 4; ++c) rv[T][c] = lds_read_tr8_at((st_lds | tr_off[c]) ^ (uint32_t)(T << 5));
-      }
+          for (int r = 0; r < 2; ++r) {
+            const int row = r == 0 ? row0 : row1;
+            if (row < a.R) {
+              const v4f gl = r == 0 ? gl0 : gl1;
+              const float lfin = gl[1];
+              const bool empty = !(lfin > 0.0f);
+              float inv = empty ? 0.0f : 1.0f / lfin;
+              if (cur_bad) inv = nanv;
+              float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
 #pragma unroll
-      for (int T = 0; T < 4; ++T) {
-        O[2 * T] *= gam0;
-        O[2 * T + 1] *= gam1;
-      }
+              for (int T = 0; T < 4; ++T) {
 #pragma unroll
-      for (int T = 0; T < 4; ++T) {
-        const v8i A = v8i{rv[T][0][0], rv[T][0][1], rv[T][1][0], rv[T][1][1],
-                          rv[T][2][0], rv[T][2][1], rv[T][3][0], rv[T][3][1]};
-        O[2 * T] = mfma_f8_32x32x64(A, P0, O[2 * T]);
-        O[2 * T + 1] = mfma_f8_32x32x64(A, P1, O[2 * T + 1]);
-      }
-      // ---- end of a piece: write the normalized partial output and LSE ------
-      // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
-      if (k == nblocks || gstart + k >= cur_end) {
-        const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
-                                                : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
-        const float nanv = __builtin_nanf("");
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-          const int row = r == 0 ? row0 : row1;
-          if (row < a.R) {
-            const v4f gl = r == 0 ? gl0 : gl1;
-            const float lfin = gl[1];
-            const bool empty = !(lfin > 0.0f);
-            float inv = empty ? 0.0f : 1.0f / lfin;
-            if (cur_bad) inv = nanv;
-            float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
-#pragma unroll
-            for (int T = 0; T < 4; ++T) {
-#pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
-                    v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
-                        O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
-                __builtin_amdgcn_sched_barrier(0);
+                for (int q = 0; q < 4; ++q) {
+                  *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
+                      v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
+                          O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
+                  __builtin_amdgcn_sched_barrier(0);
+                }
+              }
+              if (dq == 0 && h == 0) {
+                float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
+                if (cur_bad) lse = nanv;
+                a.part_lse[pid * a.rows_pad + row] = lse;
               }
             }
-            if (dq == 0 && h == 0) {
-              float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
-              if (cur_bad) lse = nanv;
-              a.part_lse[pid * a.rows_pad + row] = lse;
-            }
           }
-        }
 #pragma unroll
-        for (int T = 0; T < 8; ++T) O[T] = v16f{0};
+          for (int T = 0; T < 8; ++T) O[T] = v16f{0};
+        }
       }
       if (k == nblocks) break;
-      // piece bookkeeping for block k (mirrors the QK waves)
+
+      // ---- block k: piece bookkeeping (mirrors the QK waves) -----------------
       const int gb = gstart + k;
       if (gb >= cur_end) {
         enter_piece(gb);
         cur_bad = false;
       }
       cur_bad |= ((stage_bad >> (k % kLatStages)) & 1u) != 0;
-      prev_valid = min(kPage, cur_n - (gb - cur_p0) * kPage);
+      const int valid = min(kPage, cur_n - (gb - cur_p0) * kPage);
+      uint8_t* stp = smem + (k % kLatStages) * kLatBytes;
+      if (valid < kPage) {
+        // last page of a sequence: clear the bytes of the slots past its end that
+        // this wave reads (stale data could hold NaN codes; their probability
+        // codes are 0).  The QK waves mask these slots whatever they hold.
+        const int nz = (kPage - valid) * 8;
+        for (int i = lane; i < nz; i += 64) {
+          const int t = valid + (i >> 3);
+          const int c = 8 * dq + (i & 7);
+          *reinterpret_cast<v4i*>(stp + t * kDc + ((c ^ swz(t)) << 4)) = v4i{0, 0, 0, 0};
+        }
+      }
+      // V^T tiles of block k
+      const uint32_t st_lds = smem_base + (k % kLatStages) * kLatBytes;
+#pragma unroll
+      for (int T = 0; T < 4; ++T) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) rv[T][c] = lds_read_tr8_at((st_lds | tr_off[c]) ^ (uint32_t)(T << 5));
+      }
+      // codes and state of block k, once all four QK waves have published them
+      for (int spin = 0; spin < kSpinLimit; ++spin) {
+        const v4i f4 = flag_load4(xf);
+        if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
+      }
+      asm volatile("" ::: "memory");
+      gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
+      gl1 = *reinterpret_cast<const v4f*>(xg + (n + 32) * 4);
+      // B operand of row tile r: bytes 32h .. 32h+31 of row 32r + n (the K order
+      // of the PV product, see the transposed reads)
+      const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h);
+      const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h + 16);
+      const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h);
+      const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h + 16);
+      P0 = v8i{c00[0], c00[1], c00[2], c00[3], c01[0], c01[1], c01[2], c01[3]};
+      P1 = v8i{c10[0], c10[1], c10[2], c10[3], c11[0], c11[1], c11[2], c11[3]};
+      const int pg_next = pg_ring_p[(k + 4) & 3];   // id of block k+4 (stale when not copied)
+      lds_wait_all();
+      pg_lat = __builtin_amdgcn_readfirstlane(pg_next);
     }
   }
 }

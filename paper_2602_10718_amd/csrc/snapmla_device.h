@@ -39,6 +39,17 @@ __device__ __forceinline__ int cvt_pk_e4m3(float a, float b, int old, bool hi) {
 
 __device__ __forceinline__ float clamp448(float x) { return fminf(fmaxf(x, -kFp8Max), kFp8Max); }
 
+// 16x16x128 FP8 MFMA: lane (i%16, i/16) holds A[i%16][32*(i/16) + 0..31] and
+// B[32*(i/16) + 0..31][i%16]; C lane i register v is C[4*(i/16) + v][i%16].
+__device__ __forceinline__ v4f mfma_f8_16x16x128(v8i a, v8i b, v4f c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// 16x16x32 BF16 MFMA: lane (i%16, i/16) holds K = 8*(i/16) + 0..7; same C layout.
+__device__ __forceinline__ v4f mfma_bf16_16x16x32(v4i a, v4i b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a), __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+}
+
 // 32x32x64 FP8 (E4M3 x E4M3) MFMA, float32 accumulate.  Lane (i%32, i/32) holds
 // A[i%32][32*(i/32) + 0..31] and B[32*(i/32) + 0..31][i%32]; C lane i register v is
 // C[8*(v/4) + 4*(i/32) + v%4][i%32].
@@ -59,6 +70,18 @@ __device__ __forceinline__ float xhalf_max(float x) {
 }
 __device__ __forceinline__ float xhalf_sum(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Maximum / sum over the four lanes i, i^16, i^32, i^48 (one row of a 16x16 tile).
+__device__ __forceinline__ float quad_max(float x) {
+  x = xhalf_max(x);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float quad_sum(float x) {
+  x = xhalf_sum(x);
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
