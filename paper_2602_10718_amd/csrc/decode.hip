@@ -77,6 +77,10 @@ constexpr float kLn2 = 0.69314718055994531f;
 // Upper bound on the polls of a handshake wait.  The waits end by construction
 // (every flag they poll is stored once per block, before its owner waits on
 // anything); the bound only guarantees that the kernel terminates.
+// store instructions of one PV wave at the end of a piece: 2 row tiles x
+// (16 output chunks + 1 log-sum-exp)
+constexpr int kPieceStores = 2 * (16 + 1);
+static_assert(20 + kPieceStores < 64, "wait counter range");
 constexpr int kSpinLimit = 1 << 22;
 
 // Latent rows are stored with 16-byte chunk c of token t at chunk c ^ swz(t),
@@ -151,14 +155,23 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
 
   // piece bookkeeping (identical in every wave; scalar)
   int cur_b = -1, cur_blk0 = 0, cur_end = 0, cur_n = 0, cur_p0 = 0;
+  // (the three loads of the usual case, the next sequence, are issued together:
+  // one memory round trip per piece; only sequences without blocks loop)
   auto enter_piece = [&](int gb) {
     int b = cur_b < 0 ? find_seq(prefix, a.B, gb) : cur_b + 1;
-    while (prefix[b + 1] <= gb) ++b;
+    int p0 = prefix[b], p1 = prefix[b + 1], nb = seq_lens[b];
+    asm volatile("" ::"s"(nb));                   // keeps the length load beside the prefix loads
+    while (p1 <= gb) {
+      ++b;
+      p0 = p1;
+      p1 = prefix[b + 1];
+      nb = seq_lens[b];
+    }
     cur_b = b;
-    cur_p0 = prefix[b];
-    cur_blk0 = gb - cur_p0;
-    cur_end = prefix[b + 1];
-    cur_n = seq_lens[b];
+    cur_p0 = p0;
+    cur_blk0 = gb - p0;
+    cur_end = p1;
+    cur_n = nb;
   };
 
   if (is_qk && lane == 0) flag_store(xf + w, 0);   // ordered before any wait by the first barrier
@@ -443,13 +456,14 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     }
     // Top-of-period wait: block k (latent and RoPE) complete, and the page id
     // read at the end of the period.  Loads complete in issue order: in steady
-    // state the RoPE copy of block k is followed by the latent copy of block k+1
-    // and the 12 requests of period k-1, so "at most 20 outstanding" suffices
-    // (19 in period 0, after the prologue); the period's stores, issued after its
-    // copies, only make the wait stricter.
-    auto top_barrier = [&](int k) {
+    // state the RoPE copy of block k is followed by the latent copy of block k+1,
+    // the piece-end stores of period k-1 if any (kPieceStores of them) and its 12
+    // requests, so "at most 20 (+ kPieceStores) outstanding" suffices; 19 in
+    // period 0, after the prologue.
+    auto top_barrier = [&](int k, bool after_stores) {
       if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
       else if (k == 0) barrier_vm_lgkm0<19>();
+      else if (after_stores) barrier_vm_lgkm0<20 + kPieceStores>();
       else barrier_vm_lgkm0<20>();
     };
 
@@ -457,14 +471,10 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     v8i P0, P1;                   // its codes, row tiles 0 and 1
     v4f gl0, gl1;                 // its per-row state {gamma, l, m, sigma_P}
     bool cur_bad = false;
+    bool stored = false;          // the previous period wrote piece results
     for (int k = 0;; ++k) {
-      top_barrier(k);
-      if (k + 2 < nblocks) {
-        request_page(k + 6);
-        copy_rope_scale(k + 2, pg_rope);
-        copy_latent(k + 3, pg_lat);
-        pg_rope = pg_lat;
-      }
+      top_barrier(k, stored);
+      stored = false;
       if (k > 0) {
         // ---- PV of block k-1 --------------------------------------------------
 #pragma unroll
@@ -485,36 +495,48 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
                                                   : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
           const float nanv = __builtin_nanf("");
+          // Exactly kPieceStores store instructions per wave, whatever R: rows up to
+          // rows_pad lie inside the piece's slot (the combine reads rows < R only),
+          // and every wave writes the same LSE values.  The next top-of-period wait
+          // counts them.
 #pragma unroll
           for (int r = 0; r < 2; ++r) {
             const int row = r == 0 ? row0 : row1;
-            if (row < a.R) {
-              const v4f gl = r == 0 ? gl0 : gl1;
-              const float lfin = gl[1];
-              const bool empty = !(lfin > 0.0f);
-              float inv = empty ? 0.0f : 1.0f / lfin;
-              if (cur_bad) inv = nanv;
-              float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
+            const v4f gl = r == 0 ? gl0 : gl1;
+            const float lfin = gl[1];
+            const bool empty = !(lfin > 0.0f);
+            float inv = empty ? 0.0f : 1.0f / lfin;
+            if (cur_bad) inv = nanv;
+            float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
 #pragma unroll
-              for (int T = 0; T < 4; ++T) {
+            for (int T = 0; T < 4; ++T) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                  *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
-                      v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
-                          O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
-                  __builtin_amdgcn_sched_barrier(0);
-                }
-              }
-              if (dq == 0 && h == 0) {
-                float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
-                if (cur_bad) lse = nanv;
-                a.part_lse[pid * a.rows_pad + row] = lse;
+              for (int q = 0; q < 4; ++q) {
+                *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
+                    v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
+                        O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
+                __builtin_amdgcn_sched_barrier(0);
               }
             }
+            if (h == 0) {
+              float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
+              if (cur_bad) lse = nanv;
+              a.part_lse[pid * a.rows_pad + row] = lse;
+            }
+            __builtin_amdgcn_sched_barrier(0);
           }
 #pragma unroll
           for (int T = 0; T < 8; ++T) O[T] = v16f{0};
+          stored = true;
         }
+      }
+      // copies after the products and the piece-end stores, so that the stores
+      // precede the period's copies in the wait counter
+      if (k + 2 < nblocks) {
+        request_page(k + 6);
+        copy_rope_scale(k + 2, pg_rope);
+        copy_latent(k + 3, pg_lat);
+        pg_rope = pg_lat;
       }
       if (k == nblocks) break;
 
