@@ -40,21 +40,25 @@ def _log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def _src_hash():
+SOURCES_OF = {"decode": ("decode.hip", "quant.hip", "snapmla_device.h"),
+              "fetch_dequant": ("fetch.hip", "snapmla_device.h")}
+
+
+def _src_hash(op="decode"):
     h = hashlib.sha256()
-    for f in ("decode.hip", "quant.hip", "snapmla_device.h"):
+    for f in SOURCES_OF[op]:
         h.update(open(os.path.join(ROOT, "paper_2602_10718_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def _traffic(workload_name):
-    """HBM bytes per decode call measured with rocprofv3 counters (profiles/), if still current."""
+def _traffic(key, op="decode"):
+    """HBM bytes per launch measured with rocprofv3 counters (profiles/), if the sources still match."""
     try:
         d = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    e = d.get(workload_name)
-    if not e or e.get("src_hash") != _src_hash():
+    e = d.get(key)
+    if not e or e.get("src_hash") != _src_hash(op):
         return None
     return e.get("hbm_bytes_per_launch")
 
@@ -91,6 +95,122 @@ def cpu_baseline(w, budget_s=15.0):
                       f"{el * w.total_tokens / toks:.1f} s"}
 
 
+FETCH_BYTES_PER_TOKEN = BYTES_PER_TOKEN + 2 * (512 + 64)     # cache row read + bf16 row written
+
+
+def fetch_cpu_baseline(w, run, budget_s=10.0):
+    """The oracle's fetch_dequant, as written, on whole sequences of the device cache until ~budget_s."""
+    import torch
+    from oracle import fetch
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    el, toks, seqs = 0.0, 0, 0
+    for b in range(w.B):
+        n = int(w.seq_lens[b])
+        npg = (n + 63) // 64
+        pages = run.page_table[b, :npg].long()
+        lat = run.kv_latent[pages].cpu().numpy()
+        sc = run.kv_scale[pages].cpu().numpy()
+        rope = run.k_rope[pages].view(torch.int16).cpu().numpy().view("uint16")
+        import numpy as np
+        pt = np.arange(npg, dtype=np.int32)[None]
+        ts = time.perf_counter()
+        fetch.fetch_dequant(lat, sc, rope, pt, np.array([0, n]))
+        el += time.perf_counter() - ts
+        toks += n
+        seqs += 1
+        if el > budget_s and seqs >= 2:
+            break
+    return {"value": round(toks * FETCH_BYTES_PER_TOKEN / el / 1e9, 3), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{seqs} of {w.B} sequences ({toks} tokens): oracle fetch_dequant over pages read back from "
+                      f"the device cache, {el:.1f} s"}
+
+
+def bench_fetch(args, w, run):
+    """snapmla_fetch_dequant over every cached token of the workload (one launch per call)."""
+    import numpy as np
+    import torch
+    from paper_2602_10718_amd import snapmla as sm
+    run.append()                       # the step's tokens too: every counted token is in the cache
+    torch.cuda.synchronize()
+    cu = np.concatenate([[0], np.cumsum(w.seq_lens)]).astype(np.int32)
+    cu_d = torch.from_numpy(cu).cuda()
+    out = torch.empty((int(cu[-1]), 576), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def call():
+        sm.snapmla_fetch_dequant(run.kv_latent, run.kv_scale, run.k_rope, run.page_table, cu_d, out)
+
+    if args.traffic_probe:
+        src = torch.ones(1 << 26, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            call()
+            torch.cuda.synchronize()
+        print(json.dumps({"traffic_probe": True, "op": "fetch_dequant", "copy_bytes_read": src.numel() * 4,
+                          "calls": 3, "tokens": int(cu[-1])}), flush=True)
+        return
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(args.steps):
+        call()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    nbytes = int(cu[-1]) * FETCH_BYTES_PER_TOKEN
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    _log(f"fetch_dequant: {ms * 1e3:.1f} us/call, {gbps:.0f} GB/s")
+    # context: a plain device copy moving the same number of bytes (half read, half written)
+    src = torch.empty(nbytes // 2 // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    b.record(stream)
+    torch.cuda.synchronize()
+    copy_ms = a.elapsed_time(b) / 10
+    del src, dst
+    copy_ref = {"bytes": nbytes // 2 // 4 * 4 * 2, "us": round(copy_ms * 1e3, 1),
+                "GBps": round(nbytes / (copy_ms * 1e-3) / 1e9, 1)}
+    _log(f"device copy of the same bytes: {copy_ref}")
+    line = {
+        "metric": "fetch-dequant GB/s (644 B read + 1152 B written per cached token)",
+        "value": round(gbps, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "us_per_step": round(ms * 1e3, 1), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "e4m3->bf16", "data": "synthetic",
+        "config": {"workload": wl_names()[args.config] + " cache, every token fetched", "tokens": int(cu[-1]),
+                   "sequences": w.B, "bytes_per_call": nbytes, "step": "snapmla_fetch_dequant"},
+        "roofline": {"bound": "hbm", "kernel": "fetch_dequant_kernel, HIP events on its stream",
+                     "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": _traffic("fetch_" + w.name, "fetch_dequant"),
+                     "algorithmic_bytes_per_launch": nbytes},
+        "device_copy_same_bytes": copy_ref,
+    }
+    if not args.no_cpu_baseline:
+        _log("cpu baseline (oracle) ...")
+        line["cpu_baseline"] = fetch_cpu_baseline(w, run)
+    print(json.dumps(line), flush=True)
+
+
+def wl_names():
+    from paper_2602_10718_amd import workloads as wl
+    return wl.CONFIG_NAMES
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,6 +220,9 @@ def main():
     ap.add_argument("--num-splits", type=int, default=None)
     ap.add_argument("--cold-steps", type=int, default=20, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant"],
+                    help="decode: the hot path step (default); fetch_dequant: snapmla_fetch_dequant over every "
+                         "cached token of the workload")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: one 256 MiB device copy (counter calibration), then 3 "
                          "snapmla_decode calls; prints what it ran and exits")
@@ -122,6 +245,10 @@ def main():
     _log(f"cache filled ({w.total_tokens} tokens) in {t_fill:.1f} s")
     stream = torch.cuda.current_stream()
     kv_bytes = w.kv_bytes()
+
+    if args.op == "fetch_dequant":
+        bench_fetch(args, w, run)
+        return
 
     if args.traffic_probe:
         src = torch.ones(1 << 26, dtype=torch.float32, device="cuda")
@@ -202,7 +329,7 @@ def main():
 
     gbps = kv_bytes / (ms_per_step * 1e-3) / 1e9
     decode_gbps = kv_bytes / (decode_us * 1e-6) / 1e9
-    traffic = _traffic(w.name)
+    traffic = _traffic(w.name, "decode")
     line = {
         "metric": METRIC,
         "value": round(gbps, 1),

@@ -181,6 +181,31 @@ int snapmla_combine(const void* workspace, size_t workspace_bytes, const int32_t
                     hipStream_t stream);
 
 /*
+ * snapmla_fetch_dequant -- fused fetch-and-dequantize of the paged cache into
+ * BF16 rows (Section 3.3, Fused-Fetch-Dequant: for phases that reuse the cache
+ * at high precision, such as chunk prefill or prefix caching; the FP8 rows are
+ * dequantized in registers right after the load, in one pass).
+ *
+ * Sequence b has cu_seqlens[b+1] - cu_seqlens[b] cached tokens (its tokens
+ * 0, 1, ...); token j is written to output row cu_seqlens[b] + j:
+ *     out[row][0:512]   = bf16( fp32( E4M3(code_i) * sigma_K ) )   (round to nearest even)
+ *     out[row][512:576] = the token's RoPE key, bit for bit
+ * Every token whose page id is outside [0, num_pages), and every token of a
+ * sequence longer than max_pages * 64, gets a row of bf16 NaN (0x7FC0).
+ * Sequences with cu_seqlens[b+1] <= cu_seqlens[b] write nothing.
+ *
+ *   kv_latent, kv_scale, k_rope, page_table   cache (layout above), device, read
+ *   cu_seqlens  int32 [B+1]        device, read: output row offsets (nondecreasing)
+ *   out         bf16 [cu_seqlens[B]][576]   device, written (the caller sizes it
+ *                                            from cu_seqlens[B]; only those rows are written)
+ *   0 <= B <= 65535, max_pages >= 1, num_pages >= 1, page_size == 64
+ */
+int snapmla_fetch_dequant(const uint8_t* kv_latent, const float* kv_scale, const void* k_rope,
+                          const int32_t* page_table, const int32_t* cu_seqlens,
+                          int32_t B, int32_t max_pages, int32_t num_pages, int32_t page_size,
+                          void* out, hipStream_t stream);
+
+/*
  * snapmla_e4m3_encode -- test hook: E4M3 codes of n float32 values through the
  * same device conversion the quantizers use (round to nearest even, values at
  * or beyond 464 in magnitude saturate to +-448).  x, codes: device; n >= 0.

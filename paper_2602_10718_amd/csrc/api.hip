@@ -233,4 +233,31 @@ int snapmla_combine(const void* workspace, size_t workspace_bytes, const int32_t
   return hip_status(snapmla::launch_combine(c, stream), "combine launch");
 }
 
+int snapmla_fetch_dequant(const uint8_t* kv_latent, const float* kv_scale, const void* k_rope,
+                          const int32_t* page_table, const int32_t* cu_seqlens, int32_t B, int32_t max_pages,
+                          int32_t num_pages, int32_t page_size, void* out, hipStream_t stream) {
+  if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
+  if (B < 0 || B > 65535) return fail(SNAPMLA_INVALID_ARGUMENT, "B must be in [0, 65535] (got %d)", B);
+  if (max_pages < 1 || num_pages < 1)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
+  if (B == 0) return ok();
+  if (!kv_latent || !kv_scale || !k_rope || !page_table || !cu_seqlens || !out)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer");
+  if (misaligned(kv_latent) || misaligned(kv_scale) || misaligned(k_rope) || misaligned(out))
+    return fail(SNAPMLA_MISALIGNED, "kv_latent, kv_scale, k_rope and out must be 16-byte aligned");
+  if (misaligned4(page_table) || misaligned4(cu_seqlens))
+    return fail(SNAPMLA_MISALIGNED, "page_table and cu_seqlens must be 4-byte aligned");
+  snapmla::FetchArgs a;
+  a.kv_latent = kv_latent;
+  a.kv_scale = kv_scale;
+  a.k_rope = static_cast<const uint16_t*>(k_rope);
+  a.page_table = page_table;
+  a.cu = cu_seqlens;
+  a.out = static_cast<uint16_t*>(out);
+  a.B = B;
+  a.max_pages = max_pages;
+  a.num_pages = num_pages;
+  return hip_status(snapmla::launch_fetch_dequant(a, stream), "fetch_dequant launch");
+}
+
 }  // extern "C"

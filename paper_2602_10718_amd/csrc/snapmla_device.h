@@ -17,6 +17,7 @@ constexpr float kFp8Max = 448.0f;
 constexpr float kEps = 9.094947017729282e-13f;  // 2^-40
 
 typedef int v2i __attribute__((ext_vector_type(2)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));

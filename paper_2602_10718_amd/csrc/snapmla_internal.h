@@ -55,6 +55,16 @@ struct CombineArgs {
   int B, q_len, H, R, rows_pad, num_splits, chunk_blocks, out_dtype;
 };
 
+struct FetchArgs {
+  const uint8_t* kv_latent;   // [num_pages][64][512]
+  const float* kv_scale;      // [num_pages][64]
+  const uint16_t* k_rope;     // [num_pages][64][64]
+  const int32_t* page_table;  // [B][max_pages]
+  const int32_t* cu;          // [B+1] output row offsets; sequence b has cu[b+1] - cu[b] tokens
+  uint16_t* out;              // [cu[B]][576] bf16
+  int B, max_pages, num_pages;
+};
+
 hipError_t launch_quantize_rows(const uint16_t* x, int64_t rows, uint8_t* codes, float* scale,
                                 hipStream_t stream);
 hipError_t launch_append(const uint16_t* c_kv_new, const uint16_t* k_rope_new, const int32_t* page_table,
@@ -64,5 +74,6 @@ hipError_t launch_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t 
 hipError_t launch_prep(const PrepArgs& a, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
+hipError_t launch_fetch_dequant(const FetchArgs& a, hipStream_t stream);
 
 }  // namespace snapmla

@@ -48,9 +48,12 @@ lib.snapmla_combine.restype = ctypes.c_int
 lib.snapmla_combine.argtypes = [_p, _sz, _p, _i32, _i32, _i32, _i32, _i32, _p, _i32, _p, _p]
 lib.snapmla_e4m3_encode.restype = ctypes.c_int
 lib.snapmla_e4m3_encode.argtypes = [_p, _i64, _p, _p]
+lib.snapmla_fetch_dequant.restype = ctypes.c_int
+lib.snapmla_fetch_dequant.argtypes = [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]
 
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
-           "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode"]
+           "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
+           "snapmla_fetch_dequant"]
 
 
 class SnapMLAError(RuntimeError):
@@ -141,3 +144,12 @@ def default_num_splits(q_len, H, device=None):
     props = torch.cuda.get_device_properties(device if device is not None else torch.cuda.current_device())
     groups = math.ceil(q_len * H / 64)
     return max(8, (props.multi_processor_count // groups) // 8 * 8)
+
+
+def snapmla_fetch_dequant(kv_latent, kv_scale, k_rope, page_table, cu_seqlens, out, page_size=64, stream=None):
+    """cu_seqlens int32 [B+1] (device); out bf16 [cu_seqlens[B], 576]: per cached token the dequantized
+    latent (512) then the RoPE key (64)."""
+    B = cu_seqlens.numel() - 1
+    _check(lib.snapmla_fetch_dequant(_ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope), _ptr(page_table),
+                                     _ptr(cu_seqlens), B, page_table.shape[1], kv_latent.shape[0], page_size,
+                                     _ptr(out), _stream(stream)))

@@ -101,3 +101,15 @@ def test_other_entry_points_validate(sm):
     assert L.snapmla_e4m3_encode(None, 5, None, None) == 1
     assert L.snapmla_combine(None, 0, None, 2, 1, 16, 8, 0, None, 3, None, None) == 1
     assert L.snapmla_combine(4096, 16, 4096, 2, 1, 16, 8, 0, 4096, 0, None, None) == 3
+
+
+def test_fetch_dequant_validates(sm):
+    L = sm.lib
+    assert L.snapmla_fetch_dequant(None, None, None, None, None, 1, 4, 4, 32, None, None) == 2    # page size
+    assert L.snapmla_fetch_dequant(None, None, None, None, None, -1, 4, 4, 64, None, None) == 1   # B < 0
+    assert L.snapmla_fetch_dequant(None, None, None, None, None, 70000, 4, 4, 64, None, None) == 1
+    assert L.snapmla_fetch_dequant(None, None, None, None, None, 2, 0, 4, 64, None, None) == 1    # max_pages
+    assert L.snapmla_fetch_dequant(None, None, None, None, None, 0, 4, 4, 64, None, None) == 0    # nothing to do
+    assert L.snapmla_fetch_dequant(None, None, None, None, None, 2, 4, 4, 64, None, None) == 1    # null pointers
+    assert L.snapmla_fetch_dequant(4104, 4096, 4096, 4096, 4096, 2, 4, 4, 64, 4096, None) == 4   # misaligned latent
+    assert L.snapmla_fetch_dequant(4096, 4096, 4096, 4098, 4096, 2, 4, 4, 64, 4096, None) == 4   # misaligned table
