@@ -206,6 +206,73 @@ def bench_fetch(args, w, run):
     print(json.dumps(line), flush=True)
 
 
+FP8_PEAK_TFLOPS = 5000.0       # dense FP8 MFMA
+BF16_PEAK_TFLOPS = 2500.0      # dense BF16 MFMA
+
+
+def bench_sweep(args):
+    """Decode + combine of the same batch-32 cache for every (H, q_len) of the sweep."""
+    import numpy as np
+    import torch
+    from paper_2602_10718_amd import workloads as wl
+    from paper_2602_10718_amd.runner import DecodeRunner
+    stream = torch.cuda.current_stream()
+    base = None
+    rows = []
+    t_fill = time.perf_counter()
+
+    def timed(fn, k):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(k):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / k * 1e3
+
+    for q_len in wl.SWEEP_QLEN:
+        for H in wl.SWEEP_HEADS:
+            w = wl.sweep(H, q_len)
+            run = DecodeRunner(w, out_dtype=torch.bfloat16,
+                               cache=None if base is None else (base.kv_latent, base.kv_scale, base.k_rope))
+            if base is None:
+                base = run
+                t_fill = time.perf_counter() - t_fill
+                _log(f"sweep cache filled ({w.total_tokens} tokens) in {t_fill:.1f} s")
+            run.append()
+            for _ in range(args.warmup):
+                run.decode()
+                run.combine()
+            us_dec = timed(run.decode, args.steps)
+            us_cmb = timed(run.combine, args.steps)
+            R = H * q_len
+            toks = w.total_tokens
+            t_hbm = w.kv_bytes() / (HBM_PEAK_GBPS * 1e9) * 1e6
+            t_mfma = toks * R * (2 * 512 * 2 / (FP8_PEAK_TFLOPS * 1e12) + 2 * 64 / (BF16_PEAK_TFLOPS * 1e12)) * 1e6
+            e = {"H": H, "q_len": q_len, "rows": R, "causal": bool(w.causal), "num_splits": run.num_splits,
+                 "decode_us": round(us_dec, 1), "combine_us": round(us_cmb, 1),
+                 "kv_GBps": round(w.kv_bytes() / (us_dec * 1e-6) / 1e9, 1),
+                 "hbm_roofline_us": round(t_hbm, 1), "mfma_roofline_us": round(t_mfma, 1),
+                 "bound": "mfma" if t_mfma > t_hbm else "hbm",
+                 "frac_hbm": round(t_hbm / us_dec, 4), "frac_mfma": round(t_mfma / us_dec, 4)}
+            e["frac"] = max(e["frac_hbm"], e["frac_mfma"])
+            rows.append(e)
+            _log(f"H={H} q_len={q_len}: decode {us_dec:.1f} us ({e['kv_GBps']} GB/s, {e['bound']} frac {e['frac']})")
+            del run
+    w = wl.sweep(64, 1)
+    line = {"metric": "sensitivity sweep: snapmla_decode us and roofline fraction per (H, q_len)",
+            "unit": "us", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": False,
+            "dtype": "e4m3", "data": "synthetic",
+            "config": {"workload": "batch 32, lengths U[16384, 131072], shared cache", "batch": w.B,
+                       "kv_tokens": w.total_tokens, "kv_bytes": w.kv_bytes(), "heads": list(wl.SWEEP_HEADS),
+                       "q_len": list(wl.SWEEP_QLEN), "peaks": {"hbm_GBps": HBM_PEAK_GBPS,
+                                                               "fp8_TFLOPs": FP8_PEAK_TFLOPS,
+                                                               "bf16_TFLOPs": BF16_PEAK_TFLOPS}},
+            "sweep": rows}
+    print(json.dumps(line), flush=True)
+
+
 def wl_names():
     from paper_2602_10718_amd import workloads as wl
     return wl.CONFIG_NAMES
@@ -220,9 +287,10 @@ def main():
     ap.add_argument("--num-splits", type=int, default=None)
     ap.add_argument("--cold-steps", type=int, default=20, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant"],
+    ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant", "sweep"],
                     help="decode: the hot path step (default); fetch_dequant: snapmla_fetch_dequant over every "
-                         "cached token of the workload")
+                         "cached token of the workload; sweep: decode + combine for H in 16..128 x q_len in {1, 2} "
+                         "at batch 32, lengths U[16K, 128K]")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: one 256 MiB device copy (counter calibration), then 3 "
                          "snapmla_decode calls; prints what it ran and exits")
@@ -238,6 +306,9 @@ def main():
     from paper_2602_10718_amd.runner import DecodeRunner
 
     torch.cuda.set_device(0)
+    if args.op == "sweep":
+        bench_sweep(args)
+        return
     w = wl.make(args.config)
     t_fill = time.perf_counter()
     run = DecodeRunner(w, num_splits=args.num_splits, out_dtype=torch.bfloat16)

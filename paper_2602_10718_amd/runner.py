@@ -31,7 +31,9 @@ class DecodeRunner:
     step's n_new); step() appends the n_new step tokens, decodes and combines.
     """
 
-    def __init__(self, wl, num_splits=None, kv_chunk_tokens=None, out_dtype=torch.float32, fill=True):
+    def __init__(self, wl, num_splits=None, kv_chunk_tokens=None, out_dtype=torch.float32, fill=True, cache=None):
+        """cache: (kv_latent, kv_scale, k_rope) of another runner over the same sequences, pages and
+        tokens, used instead of allocating and filling a new one."""
         self.wl = wl
         self.B, self.H, self.q_len = wl.B, wl.H, wl.q_len
         self.kv_chunk_tokens = wl.kv_chunk_tokens if kv_chunk_tokens is None else kv_chunk_tokens
@@ -42,9 +44,13 @@ class DecodeRunner:
                 num_splits = sm.default_num_splits(self.q_len, self.H)
         self.num_splits = num_splits
         P = wl.num_pages
-        self.kv_latent = torch.zeros((P, PAGE, D_C), dtype=torch.uint8, device="cuda")
-        self.kv_scale = torch.zeros((P, PAGE), dtype=torch.float32, device="cuda")
-        self.k_rope = torch.zeros((P, PAGE, D_R), dtype=torch.bfloat16, device="cuda")
+        if cache is not None:
+            self.kv_latent, self.kv_scale, self.k_rope = cache
+            fill = False
+        else:
+            self.kv_latent = torch.zeros((P, PAGE, D_C), dtype=torch.uint8, device="cuda")
+            self.kv_scale = torch.zeros((P, PAGE), dtype=torch.float32, device="cuda")
+            self.k_rope = torch.zeros((P, PAGE, D_R), dtype=torch.bfloat16, device="cuda")
         self.page_table = _dev(wl.page_table, torch.int32)
         self.seq_lens = _dev(wl.seq_lens, torch.int32)
         qn, qr = wl.queries()

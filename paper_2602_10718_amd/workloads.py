@@ -180,3 +180,17 @@ def custom(B, H, q_len, seq_lens, causal=False, sigma_tok=1.0, rotary=False, see
     w = Workload("custom", B, H, q_len, causal, np.asarray(seq_lens, np.int32), n_new, sigma_tok, rotary,
                  seed, kv_chunk_tokens=kv_chunk_tokens, shuffle_pages=shuffle_pages)
     return _finish(w)
+
+
+SWEEP_HEADS = (16, 32, 64, 128)
+SWEEP_QLEN = (1, 2)
+
+
+def sweep(H, q_len, seed=1100, B=32, ctx_range=(16384, 131072)):
+    """The sensitivity-sweep workload: batch 32, lengths U[16K, 128K], H heads, q_len query tokens
+    (causal when q_len == 2).  The cache content and page table depend only on the seed, B and the
+    lengths, so every (H, q_len) of the sweep reads the same cache."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0])))
+    lens = rng.integers(ctx_range[0], ctx_range[1] + 1, B).astype(np.int32)
+    w = Workload("sweep", B, H, q_len, q_len == 2, lens, q_len, 1.5, True, seed)
+    return _finish(w)
