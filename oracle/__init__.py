@@ -15,6 +15,8 @@ quant    the per-token row quantizer (Appendix C, per-token equation; the
          scale rule the paper uses for P in Algorithm 1).
 fetch    fetch-and-dequantize of the paged cache into BF16 rows (Section 3.3,
          Fused-Fetch-Dequant).
+granularity  the KV-cache quantization granularities of the accuracy ablation
+         (Appendix G, Table 3) and its three error metrics.
 mla      absorbed-mode MLA decode over per-token FP8 content + BF16 RoPE
          (Section 2 absorbed score; Section 3.2; Appendix D recurrences;
          Algorithm 1 finalisation), the split-KV log-sum-exp merge, and the
@@ -24,6 +26,6 @@ Parity status of each function is stated in its docstring; anything not
 pinned by an independent check says "parity unpinned".
 """
 
-from . import e4m3, quant, mla, fetch  # noqa: F401
+from . import e4m3, quant, mla, fetch, granularity  # noqa: F401
 
 EPS = quant.EPS

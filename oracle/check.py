@@ -31,10 +31,13 @@ from . import e4m3, mla, quant
 WINDOW = 2.0 ** -13
 
 
-def sequence_reference(qn, qr, ckv, kr, tau, q_len, H, causal, bf16=True):
+def sequence_reference(qn, qr, ckv, kr, tau, q_len, H, causal, bf16=True, cache=None):
     """Oracle results for one sequence.
 
     qn [q_len, H, 512] / qr [q_len, H, 64] / ckv [N, 512] / kr [N, 64]: uint16 bf16 bits.
+    cache: optional (codes [N, 512], scales [N], rope bits [N, 64]) the decode reads instead
+    of the per-token quantization of ckv and the raw kr (another granularity); the BF16
+    reference always uses ckv and kr.
     Returns a dict with the quantized cache (codes, scales), the oracle output and
     LSE (decode_global), its parts, and the unquantized BF16 reference.
     """
@@ -42,11 +45,15 @@ def sequence_reference(qn, qr, ckv, kr, tau, q_len, H, causal, bf16=True):
     qn = np.asarray(qn).reshape(R, 512)
     qr = np.asarray(qr).reshape(R, 64)
     q8, sq = quant.quantize_rows(qn)
-    c8, sk = quant.quantize_rows(ckv)
+    if cache is None:
+        c8, sk = quant.quantize_rows(ckv)
+        kr_c = kr
+    else:
+        c8, sk, kr_c = cache
     N = ckv.shape[0]
     vis = mla.visible_counts(N, q_len, H, causal)
-    o, lse, parts = mla.decode_global(q8, sq, qr, c8, sk, kr, tau, vis, parts=True)
-    ref = dict(q8=q8, sq=sq, qr=qr, c8=c8, sk=sk, kr=kr, vis=vis, tau=tau, o=o, lse=lse, parts=parts)
+    o, lse, parts = mla.decode_global(q8, sq, qr, c8, sk, kr_c, tau, vis, parts=True)
+    ref = dict(q8=q8, sq=sq, qr=qr, c8=c8, sk=sk, kr=kr_c, vis=vis, tau=tau, o=o, lse=lse, parts=parts)
     if bf16:
         ref["o_bf16"], ref["lse_bf16"] = mla.bf16_reference(qn, qr, ckv, kr, tau, vis)
     return ref

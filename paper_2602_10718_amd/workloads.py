@@ -59,6 +59,11 @@ class Workload:
     page_table: np.ndarray = field(default=None, repr=False)
     num_pages: int = 0
     outliers: np.ndarray = field(default=None, repr=False)
+    content_scale: float = 1.0      # multiplies every content value
+    rope_scale: float = 1.0         # multiplies every RoPE key value
+    q_rope_scale: float = 1.0       # multiplies every q_rope value
+    q_nope_scale: float = 1.0       # multiplies every q_nope value
+    outlier_gain: float = 20.0      # gain of the 4 outlier content channels
 
     @property
     def rows(self):
@@ -96,7 +101,9 @@ class Workload:
         z = rng.standard_normal((PAGE, D_C), dtype=np.float32)
         lam = np.exp(rng.standard_normal(PAGE, dtype=np.float32) * np.float32(self.sigma_tok))
         z *= lam[:, None]
-        z[:, self.outliers] *= np.float32(20.0)
+        z[:, self.outliers] *= np.float32(self.outlier_gain)
+        if self.content_scale != 1.0:
+            z *= np.float32(self.content_scale)
         if self.rotary:
             x = rng.standard_normal((PAGE, D_R), dtype=np.float32) * np.float32(2.0)
             pos = (k * PAGE + np.arange(PAGE)).astype(np.float64)
@@ -107,6 +114,8 @@ class Workload:
             r = np.concatenate([x1 * c - x2 * s, x1 * s + x2 * c], axis=1).astype(np.float32)
         else:
             r = rng.standard_normal((PAGE, D_R), dtype=np.float32)
+        if self.rope_scale != 1.0:
+            r = r * np.float32(self.rope_scale)
         return f32_to_bf16_bits(z), f32_to_bf16_bits(r)
 
     # ---- queries -----------------------------------------------------------
@@ -114,7 +123,11 @@ class Workload:
         """bf16 bits of q_nope [B, q_len, H, 512] and q_rope [B, q_len, H, 64]."""
         rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([self.seed, 2])))
         qn = rng.standard_normal((self.B, self.q_len, self.H, D_C), dtype=np.float32)
+        if self.q_nope_scale != 1.0:
+            qn = qn * np.float32(self.q_nope_scale)
         qr = rng.standard_normal((self.B, self.q_len, self.H, D_R), dtype=np.float32)
+        if self.q_rope_scale != 1.0:
+            qr = qr * np.float32(self.q_rope_scale)
         return f32_to_bf16_bits(qn), f32_to_bf16_bits(qr)
 
 
@@ -193,4 +206,15 @@ def sweep(H, q_len, seed=1100, B=32, ctx_range=(16384, 131072)):
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0])))
     lens = rng.integers(ctx_range[0], ctx_range[1] + 1, B).astype(np.int32)
     w = Workload("sweep", B, H, q_len, q_len == 2, lens, q_len, 1.5, True, seed)
+    return _finish(w)
+
+
+def ablation(B=8, H=16, ctx=4096, seed=1200):
+    """The quantization-granularity ablation workload: content around 10^0-10^1 with per-token
+    lognormal(0, 1) magnitudes and 4 outlier channels x20, RoPE keys around 10^3 (a rotary
+    rotation of N(0, var 4) vectors scaled by 250) -- the magnitude relation the paper reports for
+    real caches (content ~10^1, RoPE ~10^3).  Queries: q_nope x 0.1, q_rope x 1/50, so that the
+    logits spread over a few units and the RoPE term carries about as much as the content term."""
+    w = Workload("ablation", B, H, 1, False, np.full(B, ctx, np.int32), 1, 1.0, True, seed,
+                 content_scale=3.0, rope_scale=250.0, q_rope_scale=1.0 / 50.0, q_nope_scale=0.1)
     return _finish(w)
