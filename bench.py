@@ -273,6 +273,85 @@ def bench_sweep(args):
     print(json.dumps(line), flush=True)
 
 
+def torch_attention_f32(qn, qr, ckv, kr, tau, visible):
+    """fp32 softmax attention on bf16 inputs (device tensors, bfloat16): the unquantized reference the
+    ablation scores against.  s = tau (q_nope c^T + q_rope k_r^T); o = softmax(s) c; row r sees the
+    first visible[r] tokens.  Returns float32 [R, 512]."""
+    import torch
+    q1, q2 = qn.float(), qr.float()
+    c, k = ckv.float(), kr.float()
+    s = tau * (q1 @ c.t().contiguous() + q2 @ k.t().contiguous())
+    N = c.shape[0]
+    mask = torch.arange(N, device=s.device)[None, :] >= torch.as_tensor(visible, device=s.device)[:, None]
+    s = s.masked_fill(mask, float("-inf"))
+    return torch.softmax(s, dim=1) @ c
+
+
+def bench_ablation(args):
+    """Each cache granularity of the accuracy ablation: quantizer time, decode error vs fp32 attention."""
+    import numpy as np
+    import torch
+    from paper_2602_10718_amd import snapmla as sm
+    from paper_2602_10718_amd import workloads as wl
+    from paper_2602_10718_amd.runner import DecodeRunner
+    w = wl.ablation(B=32, H=16, ctx=8192)
+    stream = torch.cuda.current_stream()
+    run = DecodeRunner(w, out_dtype=torch.float32, fill=False)
+    T = w.total_tokens
+    ck = np.empty((T, 512), np.uint16)
+    kr = np.empty((T, 64), np.uint16)
+    cu = np.concatenate([[0], np.cumsum(w.seq_lens)]).astype(np.int32)
+    for b in range(w.B):
+        ck[cu[b]:cu[b + 1]], kr[cu[b]:cu[b + 1]] = w.tokens(b, 0, int(w.seq_lens[b]))
+    ck_d = torch.from_numpy(ck.view(np.int16)).cuda().view(torch.bfloat16)
+    kr_d = torch.from_numpy(kr.view(np.int16)).cuda().view(torch.bfloat16)
+    cu_d = torch.from_numpy(cu).cuda()
+    scratch = torch.zeros(4, dtype=torch.int32, device="cuda")
+    # the reference, once: fp32 attention on the bf16 inputs, row by row of every sequence
+    refs = []
+    for b in range(w.B):
+        vis = np.full(w.H, int(w.seq_lens[b]))
+        refs.append(torch_attention_f32(run.q_nope[b].reshape(-1, 512), run.q_rope[b].reshape(-1, 64),
+                                        ck_d[cu[b]:cu[b + 1]], kr_d[cu[b]:cu[b + 1]], w.tau, vis))
+    ref = torch.cat(refs).double()
+    rows = []
+    qbytes = T * (2 * (512 + 64) + 512 + 4 + 2 * 64)       # bf16 rows read, cache planes written
+    for name in ("snapmla", "A", "B", "C", "D"):
+        def quant():
+            sm.snapmla_quantize_cache_config(ck_d, kr_d, run.page_table, cu_d, name, run.kv_latent, run.kv_scale,
+                                             run.k_rope, scratch=scratch)
+        for _ in range(args.warmup):
+            quant()
+        torch.cuda.synchronize()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            quant()
+        e.record(stream)
+        torch.cuda.synchronize()
+        us = a.elapsed_time(e) / args.steps * 1e3
+        run.decode()
+        run.combine()
+        torch.cuda.synchronize()
+        o = run.out.reshape(-1, 512).double()
+        d = o - ref
+        cos = torch.sum(o * ref, dim=1) / (torch.linalg.norm(o, dim=1) * torch.linalg.norm(ref, dim=1))
+        r = {"config": name, "quantize_us": round(us, 1), "quantize_GBps": round(qbytes / (us * 1e-6) / 1e9, 1),
+             "rmse": float(torch.sqrt(torch.mean(d * d))), "cos_diff": float(torch.mean(1 - cos)),
+             "rel_l2": float(torch.linalg.norm(d) / torch.linalg.norm(ref))}
+        rows.append(r)
+        _log(f"{name}: quantize {us:.1f} us, rel_l2 {r['rel_l2']:.3e}, 1-cos {r['cos_diff']:.3e}, rmse {r['rmse']:.3e}")
+    line = {"metric": "KV-cache quantization granularity ablation: decode error vs fp32 attention on bf16 inputs",
+            "unit": "rel_l2", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": False,
+            "dtype": "e4m3", "data": "synthetic",
+            "config": {"workload": "ablation: B32 H16 ctx8192, content ~1e0-1e1 (x20 outliers), RoPE ~1e3",
+                       "tokens": T, "quantize_bytes_per_call": qbytes,
+                       "configs": {"snapmla": "per-token RoPE-aware", "A": "per-token RoPE-unaware",
+                                   "B": "per-tensor static 1.0", "C": "per-tensor dynamic", "D": "per-block"}},
+            "ablation": rows}
+    print(json.dumps(line), flush=True)
+
+
 def wl_names():
     from paper_2602_10718_amd import workloads as wl
     return wl.CONFIG_NAMES
@@ -287,10 +366,11 @@ def main():
     ap.add_argument("--num-splits", type=int, default=None)
     ap.add_argument("--cold-steps", type=int, default=20, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant", "sweep"],
+    ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant", "sweep", "ablation"],
                     help="decode: the hot path step (default); fetch_dequant: snapmla_fetch_dequant over every "
                          "cached token of the workload; sweep: decode + combine for H in 16..128 x q_len in {1, 2} "
-                         "at batch 32, lengths U[16K, 128K]")
+                         "at batch 32, lengths U[16K, 128K]; ablation: the cache quantized under each granularity "
+                         "of the accuracy ablation, decode error vs fp32 attention on the bf16 inputs")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: one 256 MiB device copy (counter calibration), then 3 "
                          "snapmla_decode calls; prints what it ran and exits")
@@ -308,6 +388,9 @@ def main():
     torch.cuda.set_device(0)
     if args.op == "sweep":
         bench_sweep(args)
+        return
+    if args.op == "ablation":
+        bench_ablation(args)
         return
     w = wl.make(args.config)
     t_fill = time.perf_counter()

@@ -206,6 +206,34 @@ int snapmla_fetch_dequant(const uint8_t* kv_latent, const float* kv_scale, const
                           void* out, hipStream_t stream);
 
 /*
+ * snapmla_quantize_cache_config -- the KV-cache quantizers of the accuracy
+ * ablation (Appendix G, Table 3), for measuring the decode's error under each
+ * granularity.  Writes the same cache planes as snapmla_quantize_append for a
+ * whole batch: token j of sequence b (cu_seqlens[b+1] - cu_seqlens[b] tokens) is
+ * input row cu_seqlens[b] + j and goes to page page_table[b][j / 64], slot j % 64.
+ * Every scale is max(fp32(amax / 448), 2^-40) over the configuration's group and
+ * every code E4M3_rne(fp32(x / sigma)) (IEEE float32 divisions):
+ *   config 0  per-token content, RoPE copied (the method; = quantize_append)
+ *   config 1  per-token over the 576 values of content and RoPE together; the RoPE
+ *             row stored as bf16(fp32(sigma * E4M3(r / sigma)))  (RoPE-unaware)
+ *   config 2  per-tensor static: sigma = 1 (values beyond 448 saturate)
+ *   config 3  per-tensor dynamic: one sigma from the amax of all content values
+ *   config 4  per-block: one sigma per 64-token page of a sequence
+ * Tokens past max_pages * 64 or on a page id outside [0, num_pages) are skipped.
+ *
+ *   c_kv     bf16 [cu_seqlens[B]][512], k_rope bf16 [cu_seqlens[B]][64]   device, read
+ *   page_table int32 [B][max_pages], cu_seqlens int32 [B+1]               device, read
+ *   scratch  device uint32 word used by config 3 (may be NULL otherwise); calls that
+ *            share it must not overlap
+ *   kv_latent, kv_scale, k_rope_out   cache planes, written at the batch's slots
+ *   0 <= config <= 4, 0 <= B <= 65535, max_pages >= 1, num_pages >= 1, page_size == 64
+ */
+int snapmla_quantize_cache_config(const void* c_kv, const void* k_rope, const int32_t* page_table,
+                                  const int32_t* cu_seqlens, int32_t B, int32_t max_pages, int32_t num_pages,
+                                  int32_t page_size, int32_t config, uint32_t* scratch, uint8_t* kv_latent,
+                                  float* kv_scale, void* k_rope_out, hipStream_t stream);
+
+/*
  * snapmla_e4m3_encode -- test hook: E4M3 codes of n float32 values through the
  * same device conversion the quantizers use (round to nearest even, values at
  * or beyond 464 in magnitude saturate to +-448).  x, codes: device; n >= 0.

@@ -260,4 +260,29 @@ int snapmla_fetch_dequant(const uint8_t* kv_latent, const float* kv_scale, const
   return hip_status(snapmla::launch_fetch_dequant(a, stream), "fetch_dequant launch");
 }
 
+int snapmla_quantize_cache_config(const void* c_kv, const void* k_rope, const int32_t* page_table,
+                                  const int32_t* cu_seqlens, int32_t B, int32_t max_pages, int32_t num_pages,
+                                  int32_t page_size, int32_t config, uint32_t* scratch, uint8_t* kv_latent,
+                                  float* kv_scale, void* k_rope_out, hipStream_t stream) {
+  if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
+  if (config < 0 || config > 4) return fail(SNAPMLA_INVALID_ARGUMENT, "config must be 0..4 (got %d)", config);
+  if (B < 0 || B > 65535) return fail(SNAPMLA_INVALID_ARGUMENT, "B must be in [0, 65535] (got %d)", B);
+  if (max_pages < 1 || num_pages < 1)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
+  if (B == 0) return ok();
+  if (!c_kv || !k_rope || !page_table || !cu_seqlens || !kv_latent || !kv_scale || !k_rope_out ||
+      (config == 3 && !scratch))
+    return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer");
+  if (misaligned(c_kv) || misaligned(k_rope) || misaligned(kv_latent) || misaligned(kv_scale) ||
+      misaligned(k_rope_out))
+    return fail(SNAPMLA_MISALIGNED, "c_kv, k_rope, kv_latent, kv_scale and k_rope_out must be 16-byte aligned");
+  if (misaligned4(page_table) || misaligned4(cu_seqlens) || (scratch && misaligned4(scratch)))
+    return fail(SNAPMLA_MISALIGNED, "page_table, cu_seqlens and scratch must be 4-byte aligned");
+  return hip_status(snapmla::launch_quantize_cache_config(
+                        static_cast<const uint16_t*>(c_kv), static_cast<const uint16_t*>(k_rope), page_table,
+                        cu_seqlens, B, max_pages, num_pages, config, scratch, kv_latent, kv_scale,
+                        static_cast<uint16_t*>(k_rope_out), stream),
+                    "quantize_cache_config launch");
+}
+
 }  // extern "C"

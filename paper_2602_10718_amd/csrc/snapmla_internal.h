@@ -75,5 +75,9 @@ hipError_t launch_prep(const PrepArgs& a, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_fetch_dequant(const FetchArgs& a, hipStream_t stream);
+hipError_t launch_quantize_cache_config(const uint16_t* c_kv, const uint16_t* k_rope, const int32_t* page_table,
+                                        const int32_t* cu, int B, int max_pages, int num_pages, int config,
+                                        uint32_t* amax_word, uint8_t* kv_latent, float* kv_scale,
+                                        uint16_t* k_rope_out, hipStream_t stream);
 
 }  // namespace snapmla

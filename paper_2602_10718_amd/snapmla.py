@@ -48,12 +48,16 @@ lib.snapmla_combine.restype = ctypes.c_int
 lib.snapmla_combine.argtypes = [_p, _sz, _p, _i32, _i32, _i32, _i32, _i32, _p, _i32, _p, _p]
 lib.snapmla_e4m3_encode.restype = ctypes.c_int
 lib.snapmla_e4m3_encode.argtypes = [_p, _i64, _p, _p]
+lib.snapmla_quantize_cache_config.restype = ctypes.c_int
+lib.snapmla_quantize_cache_config.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p]
 lib.snapmla_fetch_dequant.restype = ctypes.c_int
 lib.snapmla_fetch_dequant.argtypes = [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]
 
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
-           "snapmla_fetch_dequant"]
+           "snapmla_fetch_dequant", "snapmla_quantize_cache_config"]
+
+CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
 
 class SnapMLAError(RuntimeError):
@@ -153,3 +157,14 @@ def snapmla_fetch_dequant(kv_latent, kv_scale, k_rope, page_table, cu_seqlens, o
     _check(lib.snapmla_fetch_dequant(_ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope), _ptr(page_table),
                                      _ptr(cu_seqlens), B, page_table.shape[1], kv_latent.shape[0], page_size,
                                      _ptr(out), _stream(stream)))
+
+
+def snapmla_quantize_cache_config(c_kv, k_rope, page_table, cu_seqlens, config, kv_latent, kv_scale, k_rope_out,
+                                  scratch=None, page_size=64, stream=None):
+    """c_kv bf16 [T, 512], k_rope bf16 [T, 64] (token j of sequence b at row cu_seqlens[b] + j); config one of
+    CACHE_CONFIGS' names or numbers; scratch: int32 device tensor of >= 1 element (needed for config "C")."""
+    cfg = CACHE_CONFIGS[config] if isinstance(config, str) else int(config)
+    B = cu_seqlens.numel() - 1
+    _check(lib.snapmla_quantize_cache_config(_ptr(c_kv), _ptr(k_rope), _ptr(page_table), _ptr(cu_seqlens), B,
+                                             page_table.shape[1], kv_latent.shape[0], page_size, cfg, _ptr(scratch),
+                                             _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope_out), _stream(stream)))
