@@ -114,6 +114,54 @@ def bounds(ref):
     return o_bound, lse_bound, dict(delta=delta, Lstar=Lstar, tie_count=int(np.sum(tie)))
 
 
+def sequence_reference_bf16(qn, qr, ckv, kr, tau, q_len, H, causal):
+    """Oracle results of the BF16-cache decode for one sequence: float64 softmax attention on the
+    bf16 inputs themselves (mla.bf16_reference), with what bounds_bf16 needs."""
+    R = q_len * H
+    qn = np.asarray(qn).reshape(R, 512)
+    qr = np.asarray(qr).reshape(R, 64)
+    N = ckv.shape[0]
+    vis = mla.visible_counts(N, q_len, H, causal)
+    o, lse = mla.bf16_reference(qn, qr, ckv, kr, tau, vis)
+    return dict(qn=qn, qr=qr, ckv=ckv, kr=kr, tau=tau, vis=vis, o=o, lse=lse)
+
+
+def bounds_bf16(ref):
+    """Per-element output bound [R, 512] and per-row LSE bound [R] of a BF16-cache decode.
+
+    Error sources of a float32 device evaluation: the logits accumulated in float32 over 576 exact
+    bf16 products (at most 2^-16 * sum|q k| after 18 accumulation steps, plus 2^-20 |s| for the
+    scaling and the exponent); the probabilities rounded to bf16 before the PV product (relative
+    2^-8; the normalizer sums them unrounded) and the float32 rescaling and accumulation of O
+    (relative 2^-14, which covers 2^-23 per rescale for up to 2^9 rescales):
+        |do_rd| <= sum_j |dw_rj| |V_jd| + (2^-8 + 2^-14) sum_j w_rj |V_jd| + 1e-5 max|o_r|
+    with dw from the logit errors as in bounds()."""
+    Q = quant.bf16_to_f32(ref["qn"]).astype(np.float64)
+    Qr = quant.bf16_to_f32(ref["qr"]).astype(np.float64)
+    C = quant.bf16_to_f32(ref["ckv"]).astype(np.float64)
+    Kr = quant.bf16_to_f32(ref["kr"]).astype(np.float64)
+    tau = ref["tau"]
+    s = tau * (Q @ C.T + Qr @ Kr.T)
+    N = C.shape[0]
+    s = np.where(np.arange(N)[None, :] < np.asarray(ref["vis"])[:, None], s, -np.inf)
+    A = np.abs(Q) @ np.abs(C).T + np.abs(Qr) @ np.abs(Kr).T
+    fin = np.isfinite(s)
+    delta = np.where(fin, tau * 2.0 ** -16 * A + 2.0 ** -20 * np.where(fin, np.abs(s), 0.0), 0.0)
+    M = np.max(s, axis=1)
+    ok = M > -np.inf
+    e = np.where(fin, np.exp(s - np.where(ok, M, 0.0)[:, None]), 0.0)
+    lam = np.sum(e, axis=1)
+    w = np.where(ok[:, None], e / np.where(ok, lam, 1.0)[:, None], 0.0)
+    Lstar = np.log(np.maximum(np.sum(w * np.exp(np.minimum(delta, 50.0)), axis=1), 1e-300))
+    Lstar = np.where(ok, Lstar, 0.0)
+    dw = w * np.expm1(np.minimum(delta + Lstar[:, None], 50.0))
+    V = np.abs(C)
+    o_bound = dw @ V + (2.0 ** -8 + 2.0 ** -14) * (w @ V)
+    o_bound += 1e-5 * np.max(np.abs(ref["o"]), axis=1, keepdims=True) + 1e-30
+    lse_bound = Lstar + 2.0 ** -20 * np.abs(np.where(np.isfinite(ref["lse"]), ref["lse"], 0.0)) + 1e-6
+    return o_bound, lse_bound
+
+
 def metrics(o_dev, lse_dev, o_ref, lse_ref):
     """Appendix G style error metrics of o_dev against o_ref plus LSE difference."""
     o_dev = np.asarray(o_dev, np.float64)
