@@ -164,6 +164,37 @@ int snapmla_decode(const void* q_nope, const void* q_rope,
                    hipStream_t stream);
 
 /*
+ * snapmla_decode_bf16 -- the BF16-cache baseline of the paper's comparison
+ * (Section 4: the FP8 kernel against MLA decode over a BF16 cache).  Same
+ * queries, page table, split plan, workspace and combine as snapmla_decode; the
+ * cache holds bf16 latent rows and no scales:
+ *   kv_latent bf16 [num_pages][64][512], k_rope bf16 [num_pages][64][64]
+ * Per row: s = softmax_scale * (q_nope . c + q_rope . k_rope) in float32 (BF16
+ * MFMA), online softmax over 32-token blocks, P rounded to bf16 for the BF16 PV
+ * product (the normalizer sums the unrounded P), o = O / l, LSE = m + ln l.
+ * Arguments and errors as snapmla_decode (without kv_scale); complete after
+ * snapmla_combine with the same split plan.
+ */
+int snapmla_decode_bf16(const void* q_nope, const void* q_rope, const void* kv_latent, const void* k_rope,
+                        const int32_t* page_table, const int32_t* seq_lens,
+                        int32_t B, int32_t q_len, int32_t H,
+                        int32_t max_pages, int32_t num_pages, int32_t page_size,
+                        float softmax_scale, int32_t causal,
+                        int32_t num_splits, int32_t kv_chunk_tokens,
+                        void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/*
+ * snapmla_append_bf16 -- the step's new tokens into a BF16 cache (the
+ * counterpart of snapmla_quantize_append for snapmla_decode_bf16): token t of
+ * sequence b goes to position seq_lens[b] - n_new + t, its latent and RoPE rows
+ * copied bit for bit.  Arguments and skipped tokens as snapmla_quantize_append.
+ */
+int snapmla_append_bf16(const void* c_kv_new, const void* k_rope_new, const int32_t* page_table,
+                        const int32_t* seq_lens, int32_t B, int32_t n_new, int32_t max_pages, int32_t num_pages,
+                        int32_t page_size, void* kv_latent, void* k_rope, hipStream_t stream);
+
+/*
  * snapmla_combine -- split-KV log-sum-exp merge of the partial results that
  * snapmla_decode left in `workspace` (same B, q_len, H, num_splits,
  * kv_chunk_tokens and seq_lens as that call).  Per row:

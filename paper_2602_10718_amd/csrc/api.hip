@@ -51,6 +51,83 @@ int check_shapes(int32_t B, int32_t q_len, int32_t H, int32_t num_splits, int32_
   return SNAPMLA_OK;
 }
 
+// snapmla_decode and snapmla_decode_bf16: validation, workspace carve-up, the prep
+// launch (query quantization only for the FP8 cache) and the decode launch.
+int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent, const float* kv_scale,
+                  const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
+                  int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
+                  float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream, bool bf16_cache) {
+  int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (st != SNAPMLA_OK) return st;
+  if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
+  if (max_pages < 1 || num_pages < 1)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(SNAPMLA_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
+  if (causal != 0 && causal != 1) return fail(SNAPMLA_INVALID_ARGUMENT, "causal must be 0 or 1");
+  if ((int64_t)max_pages * 64 > 0x7FFFFFFF) return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages too large");
+  const snapmla::WsLayout L = snapmla::ws_layout(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (B == 0) return ok();
+  if (!q_nope || !q_rope || !kv_latent || (!bf16_cache && !kv_scale) || !k_rope || !page_table || !seq_lens ||
+      !workspace)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(q_nope) || misaligned(q_rope) || misaligned(kv_latent) || (!bf16_cache && misaligned(kv_scale)) ||
+      misaligned(k_rope) || misaligned4(page_table) || misaligned4(seq_lens) || misaligned(workspace))
+    return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
+  if (workspace_bytes < L.total)
+    return fail(SNAPMLA_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes (got %zu)", L.total, workspace_bytes);
+
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  snapmla::PrepArgs p;
+  p.q_nope = static_cast<const uint16_t*>(q_nope);
+  p.q8 = ws + L.q8;
+  p.sq = reinterpret_cast<float*>(ws + L.sq);
+  p.rows = bf16_cache ? 0 : (int64_t)B * L.R;        // the BF16 cache reads the bf16 queries as they are
+  p.seq_lens = seq_lens;
+  p.prefix = reinterpret_cast<int32_t*>(ws + L.prefix);
+  p.flags = reinterpret_cast<int32_t*>(ws + L.flags);
+  p.zero = ws + L.zero;
+  p.B = B;
+  p.q_len = q_len;
+  p.max_pages = max_pages;
+  p.chunk_blocks = kv_chunk_tokens / 64;
+  p.num_splits = num_splits;
+  hipError_t e = snapmla::launch_prep(p, stream);
+  if (e != hipSuccess) return hip_status(e, "decode prep launch");
+
+  snapmla::DecodeArgs d;
+  d.q_nope = static_cast<const uint16_t*>(q_nope);
+  d.q8 = p.q8;
+  d.sq = p.sq;
+  d.q_rope = static_cast<const uint16_t*>(q_rope);
+  d.kv_latent = static_cast<const uint8_t*>(kv_latent);
+  d.kv_scale = kv_scale;
+  d.k_rope = static_cast<const uint16_t*>(k_rope);
+  d.page_table = page_table;
+  d.seq_lens = seq_lens;
+  d.prefix = p.prefix;
+  d.zero = p.zero;
+  d.part_o = reinterpret_cast<float*>(ws + L.o);
+  d.part_lse = reinterpret_cast<float*>(ws + L.lse);
+  d.B = B;
+  d.q_len = q_len;
+  d.H = H;
+  d.R = L.R;
+  d.G = L.G;
+  d.rows_pad = L.rows_pad;
+  d.max_pages = max_pages;
+  d.num_pages = num_pages;
+  d.causal = causal;
+  d.num_splits = num_splits;
+  d.chunk_blocks = kv_chunk_tokens / 64;
+  d.sl2 = softmax_scale * 1.4426950408889634f;
+  if (bf16_cache)
+    return hip_status(snapmla::launch_decode_bf16(d, static_cast<const uint16_t*>(kv_latent), stream),
+                      "decode_bf16 launch");
+  return hip_status(snapmla::launch_decode(d, stream), "decode launch");
+}
+
 }  // namespace
 
 namespace snapmla {
@@ -135,69 +212,39 @@ int snapmla_decode(const void* q_nope, const void* q_rope, const uint8_t* kv_lat
                    int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
                    float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
-  if (st != SNAPMLA_OK) return st;
+  return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
+                       num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
+                       workspace_bytes, stream, false);
+}
+
+int snapmla_decode_bf16(const void* q_nope, const void* q_rope, const void* kv_latent, const void* k_rope,
+                        const int32_t* page_table, const int32_t* seq_lens, int32_t B, int32_t q_len, int32_t H,
+                        int32_t max_pages, int32_t num_pages, int32_t page_size, float softmax_scale,
+                        int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  return decode_common(q_nope, q_rope, kv_latent, nullptr, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
+                       num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
+                       workspace_bytes, stream, true);
+}
+
+int snapmla_append_bf16(const void* c_kv_new, const void* k_rope_new, const int32_t* page_table,
+                        const int32_t* seq_lens, int32_t B, int32_t n_new, int32_t max_pages, int32_t num_pages,
+                        int32_t page_size, void* kv_latent, void* k_rope, hipStream_t stream) {
   if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
+  if (B < 0 || n_new < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "B and n_new must be >= 0 (got %d, %d)", B, n_new);
   if (max_pages < 1 || num_pages < 1)
     return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
-  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
-    return fail(SNAPMLA_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
-  if (causal != 0 && causal != 1) return fail(SNAPMLA_INVALID_ARGUMENT, "causal must be 0 or 1");
-  if ((int64_t)max_pages * 64 > 0x7FFFFFFF) return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages too large");
-  const snapmla::WsLayout L = snapmla::ws_layout(B, q_len, H, num_splits, kv_chunk_tokens);
-  if (B == 0) return ok();
-  if (!q_nope || !q_rope || !kv_latent || !kv_scale || !k_rope || !page_table || !seq_lens || !workspace)
+  if ((int64_t)B * n_new == 0) return ok();
+  if (!c_kv_new || !k_rope_new || !page_table || !seq_lens || !kv_latent || !k_rope)
     return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
-  if (misaligned(q_nope) || misaligned(q_rope) || misaligned(kv_latent) || misaligned(kv_scale) ||
-      misaligned(k_rope) || misaligned4(page_table) || misaligned4(seq_lens) || misaligned(workspace))
-    return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
-  if (workspace_bytes < L.total)
-    return fail(SNAPMLA_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes (got %zu)", L.total, workspace_bytes);
-
-  uint8_t* ws = static_cast<uint8_t*>(workspace);
-  snapmla::PrepArgs p;
-  p.q_nope = static_cast<const uint16_t*>(q_nope);
-  p.q8 = ws + L.q8;
-  p.sq = reinterpret_cast<float*>(ws + L.sq);
-  p.rows = (int64_t)B * L.R;
-  p.seq_lens = seq_lens;
-  p.prefix = reinterpret_cast<int32_t*>(ws + L.prefix);
-  p.flags = reinterpret_cast<int32_t*>(ws + L.flags);
-  p.zero = ws + L.zero;
-  p.B = B;
-  p.q_len = q_len;
-  p.max_pages = max_pages;
-  p.chunk_blocks = kv_chunk_tokens / 64;
-  p.num_splits = num_splits;
-  hipError_t e = snapmla::launch_prep(p, stream);
-  if (e != hipSuccess) return hip_status(e, "decode prep launch");
-
-  snapmla::DecodeArgs d;
-  d.q8 = p.q8;
-  d.sq = p.sq;
-  d.q_rope = static_cast<const uint16_t*>(q_rope);
-  d.kv_latent = kv_latent;
-  d.kv_scale = kv_scale;
-  d.k_rope = static_cast<const uint16_t*>(k_rope);
-  d.page_table = page_table;
-  d.seq_lens = seq_lens;
-  d.prefix = p.prefix;
-  d.zero = p.zero;
-  d.part_o = reinterpret_cast<float*>(ws + L.o);
-  d.part_lse = reinterpret_cast<float*>(ws + L.lse);
-  d.B = B;
-  d.q_len = q_len;
-  d.H = H;
-  d.R = L.R;
-  d.G = L.G;
-  d.rows_pad = L.rows_pad;
-  d.max_pages = max_pages;
-  d.num_pages = num_pages;
-  d.causal = causal;
-  d.num_splits = num_splits;
-  d.chunk_blocks = kv_chunk_tokens / 64;
-  d.sl2 = softmax_scale * 1.4426950408889634f;
-  return hip_status(snapmla::launch_decode(d, stream), "decode launch");
+  if (misaligned(c_kv_new) || misaligned(k_rope_new) || misaligned(kv_latent) || misaligned(k_rope) ||
+      misaligned4(page_table) || misaligned4(seq_lens))
+    return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32 index arrays need 4 bytes, data buffers 16)");
+  return hip_status(snapmla::launch_append_bf16(static_cast<const uint16_t*>(c_kv_new),
+                                                static_cast<const uint16_t*>(k_rope_new), page_table, seq_lens, B,
+                                                n_new, max_pages, num_pages, static_cast<uint16_t*>(kv_latent),
+                                                static_cast<uint16_t*>(k_rope), stream),
+                    "append_bf16 launch");
 }
 
 int snapmla_combine(const void* workspace, size_t workspace_bytes, const int32_t* seq_lens, int32_t B,

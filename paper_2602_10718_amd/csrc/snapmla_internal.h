@@ -27,6 +27,7 @@ struct PrepArgs {
 };
 
 struct DecodeArgs {
+  const uint16_t* q_nope;   // [B*R][512] bf16 (read by the BF16-cache kernel only)
   const uint8_t* q8;
   const float* sq;
   const uint16_t* q_rope;   // [B*R][64]
@@ -75,6 +76,10 @@ hipError_t launch_prep(const PrepArgs& a, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream);
 hipError_t launch_fetch_dequant(const FetchArgs& a, hipStream_t stream);
+hipError_t launch_decode_bf16(const DecodeArgs& a, const uint16_t* kv_latent_bf16, hipStream_t stream);
+hipError_t launch_append_bf16(const uint16_t* c_kv_new, const uint16_t* k_rope_new, const int32_t* page_table,
+                              const int32_t* seq_lens, int B, int n_new, int max_pages, int num_pages,
+                              uint16_t* kv_latent, uint16_t* k_rope, hipStream_t stream);
 hipError_t launch_quantize_cache_config(const uint16_t* c_kv, const uint16_t* k_rope, const int32_t* page_table,
                                         const int32_t* cu, int B, int max_pages, int num_pages, int config,
                                         uint32_t* amax_word, uint8_t* kv_latent, float* kv_scale,

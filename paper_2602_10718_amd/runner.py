@@ -31,9 +31,12 @@ class DecodeRunner:
     step's n_new); step() appends the n_new step tokens, decodes and combines.
     """
 
-    def __init__(self, wl, num_splits=None, kv_chunk_tokens=None, out_dtype=torch.float32, fill=True, cache=None):
+    def __init__(self, wl, num_splits=None, kv_chunk_tokens=None, out_dtype=torch.float32, fill=True, cache=None,
+                 kv_dtype="e4m3"):
         """cache: (kv_latent, kv_scale, k_rope) of another runner over the same sequences, pages and
-        tokens, used instead of allocating and filling a new one."""
+        tokens, used instead of allocating and filling a new one.  kv_dtype "bf16": a BF16 cache
+        (kv_latent bf16, no scales) written by snapmla_append_bf16 and read by snapmla_decode_bf16."""
+        self.kv_dtype = kv_dtype
         self.wl = wl
         self.B, self.H, self.q_len = wl.B, wl.H, wl.q_len
         self.kv_chunk_tokens = wl.kv_chunk_tokens if kv_chunk_tokens is None else kv_chunk_tokens
@@ -47,6 +50,10 @@ class DecodeRunner:
         if cache is not None:
             self.kv_latent, self.kv_scale, self.k_rope = cache
             fill = False
+        elif kv_dtype == "bf16":
+            self.kv_latent = torch.zeros((P, PAGE, D_C), dtype=torch.bfloat16, device="cuda")
+            self.kv_scale = None
+            self.k_rope = torch.zeros((P, PAGE, D_R), dtype=torch.bfloat16, device="cuda")
         else:
             self.kv_latent = torch.zeros((P, PAGE, D_C), dtype=torch.uint8, device="cuda")
             self.kv_scale = torch.zeros((P, PAGE), dtype=torch.float32, device="cuda")
@@ -82,17 +89,30 @@ class DecodeRunner:
             for t0 in range(0, max(N, 0), chunk):
                 t1 = min(N, t0 + chunk)
                 ck, kr = wl.tokens(b, t0, t1)
-                sm.snapmla_quantize_append(_u16_to_bf16(ck[None]), _u16_to_bf16(kr[None]),
-                                           self.page_table[b:b + 1].clone(),
-                                           torch.tensor([t1], dtype=torch.int32, device="cuda"),
-                                           wl.num_pages, self.kv_latent, self.kv_scale, self.k_rope)
+                pt = self.page_table[b:b + 1].clone()
+                sl = torch.tensor([t1], dtype=torch.int32, device="cuda")
+                if self.kv_dtype == "bf16":
+                    sm.snapmla_append_bf16(_u16_to_bf16(ck[None]), _u16_to_bf16(kr[None]), pt, sl, wl.num_pages,
+                                           self.kv_latent, self.k_rope)
+                else:
+                    sm.snapmla_quantize_append(_u16_to_bf16(ck[None]), _u16_to_bf16(kr[None]), pt, sl,
+                                               wl.num_pages, self.kv_latent, self.kv_scale, self.k_rope)
         torch.cuda.synchronize()
 
     def append(self, stream=None):
+        if self.kv_dtype == "bf16":
+            sm.snapmla_append_bf16(self.new_ckv, self.new_krope, self.page_table, self.seq_lens, self.wl.num_pages,
+                                   self.kv_latent, self.k_rope, stream=stream)
+            return
         sm.snapmla_quantize_append(self.new_ckv, self.new_krope, self.page_table, self.seq_lens, self.wl.num_pages,
                                    self.kv_latent, self.kv_scale, self.k_rope, stream=stream)
 
     def decode(self, stream=None):
+        if self.kv_dtype == "bf16":
+            sm.snapmla_decode_bf16(self.q_nope, self.q_rope, self.kv_latent, self.k_rope, self.page_table,
+                                   self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits,
+                                   self.kv_chunk_tokens, self.workspace, stream=stream)
+            return
         sm.snapmla_decode(self.q_nope, self.q_rope, self.kv_latent, self.kv_scale, self.k_rope, self.page_table,
                           self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits, self.kv_chunk_tokens,
                           self.workspace, stream=stream)
@@ -107,10 +127,15 @@ class DecodeRunner:
         self.combine(stream)
 
     def sequence_cache(self, b):
-        """(codes uint8 [N, 512], scales f32 [N], rope bits uint16 [N, 64]) of sequence b read back via the page table."""
+        """(codes uint8 [N, 512], scales f32 [N], rope bits uint16 [N, 64]) of sequence b read back via the page table;
+        for a BF16 cache (latent bits uint16 [N, 512], None, rope bits)."""
         N = int(self.wl.seq_lens[b])
         npg = (N + PAGE - 1) // PAGE
         pages = self.page_table[b, :npg].long()
+        if self.kv_dtype == "bf16":
+            lat = self.kv_latent[pages].reshape(-1, D_C)[:N].view(torch.int16).cpu().numpy().view(np.uint16)
+            rope = self.k_rope[pages].reshape(-1, D_R)[:N].view(torch.int16).cpu().numpy().view(np.uint16)
+            return lat, None, rope
         codes = self.kv_latent[pages].reshape(-1, D_C)[:N].cpu().numpy()
         scales = self.kv_scale[pages].reshape(-1)[:N].cpu().numpy()
         rope = self.k_rope[pages].reshape(-1, D_R)[:N].view(torch.int16).cpu().numpy().view(np.uint16)

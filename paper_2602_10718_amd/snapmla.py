@@ -50,12 +50,17 @@ lib.snapmla_e4m3_encode.restype = ctypes.c_int
 lib.snapmla_e4m3_encode.argtypes = [_p, _i64, _p, _p]
 lib.snapmla_quantize_cache_config.restype = ctypes.c_int
 lib.snapmla_quantize_cache_config.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p]
+lib.snapmla_decode_bf16.restype = ctypes.c_int
+lib.snapmla_decode_bf16.argtypes = [_p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
+                                    _i32, _p, _sz, _p]
+lib.snapmla_append_bf16.restype = ctypes.c_int
+lib.snapmla_append_bf16.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p]
 lib.snapmla_fetch_dequant.restype = ctypes.c_int
 lib.snapmla_fetch_dequant.argtypes = [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]
 
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
-           "snapmla_fetch_dequant", "snapmla_quantize_cache_config"]
+           "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -168,3 +173,22 @@ def snapmla_quantize_cache_config(c_kv, k_rope, page_table, cu_seqlens, config, 
     _check(lib.snapmla_quantize_cache_config(_ptr(c_kv), _ptr(k_rope), _ptr(page_table), _ptr(cu_seqlens), B,
                                              page_table.shape[1], kv_latent.shape[0], page_size, cfg, _ptr(scratch),
                                              _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope_out), _stream(stream)))
+
+
+def snapmla_decode_bf16(q_nope, q_rope, kv_latent, k_rope, page_table, seq_lens, softmax_scale, causal, num_splits,
+                        kv_chunk_tokens, workspace, page_size=64, stream=None):
+    """kv_latent bf16 [num_pages, 64, 512]; otherwise as snapmla_decode (without kv_scale)."""
+    B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
+    _check(lib.snapmla_decode_bf16(_ptr(q_nope), _ptr(q_rope), _ptr(kv_latent), _ptr(k_rope), _ptr(page_table),
+                                   _ptr(seq_lens), B, q_len, H, page_table.shape[1], kv_latent.shape[0], page_size,
+                                   float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def snapmla_append_bf16(c_kv_new, k_rope_new, page_table, seq_lens, num_pages, kv_latent, k_rope, page_size=64,
+                        stream=None):
+    """c_kv_new bf16 [B, n_new, 512], k_rope_new bf16 [B, n_new, 64] into kv_latent bf16 [num_pages, 64, 512]."""
+    B, n_new = c_kv_new.shape[0], c_kv_new.shape[1]
+    _check(lib.snapmla_append_bf16(_ptr(c_kv_new), _ptr(k_rope_new), _ptr(page_table), _ptr(seq_lens), B, n_new,
+                                   page_table.shape[1], num_pages, page_size, _ptr(kv_latent), _ptr(k_rope),
+                                   _stream(stream)))

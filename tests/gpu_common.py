@@ -50,3 +50,36 @@ def check_sequence(run, b, ref, strict_north_star=True, label=""):
     if strict_north_star:
         assert m["rel_l2"] <= 1e-2, f"{label}: rel L2 {m['rel_l2']:.3g} > 1e-2"
     return m
+
+
+def reference_bf16(wl, b, qn=None, qr=None):
+    """Oracle results of the BF16-cache decode for sequence b of workload wl."""
+    if qn is None:
+        qn, qr = wl.queries()
+    N = int(wl.seq_lens[b])
+    ck, kr = wl.tokens(b, 0, N)
+    return check.sequence_reference_bf16(qn[b], qr[b], ck, kr, wl.tau, wl.q_len, wl.H, wl.causal)
+
+
+def check_sequence_bf16(run, b, ref, label=""):
+    """Device output/LSE of sequence b of a BF16-cache run against the oracle and its bounds."""
+    R = run.q_len * run.H
+    o = run.out[b].reshape(R, 512).float().cpu().numpy().astype(np.float64)
+    lse = run.lse[b].reshape(R).cpu().numpy().astype(np.float64)
+    ob, lb = check.bounds_bf16(ref)
+    fin = np.isfinite(ref["lse"])
+    assert np.array_equal(np.isfinite(lse), fin), f"{label}: LSE finiteness differs"
+    assert np.all(lse[~fin] == -np.inf) and np.all(o[~fin] == 0), f"{label}: rows without tokens must be 0/-inf"
+    assert np.all(np.isfinite(o)), f"{label}: non-finite output"
+    err = np.abs(o - ref["o"])
+    m = check.metrics(o, lse, ref["o"], ref["lse"])
+    m["bound_violations"] = int(np.sum(err > ob))
+    m["lse_violations"] = int(np.sum(np.abs(lse - ref["lse"])[fin] > lb[fin]))
+    print(f"[{label} b={b}] " + " ".join(f"{k}={v:.3g}" if isinstance(v, float) else f"{k}={v}"
+                                         for k, v in m.items()), flush=True)
+    worst = np.unravel_index(np.argmax(err - ob), err.shape)
+    assert m["bound_violations"] == 0, f"{label}: {m['bound_violations']} outputs outside the bound; worst at " \
+        f"{worst}: err {err[worst]:.3g} bound {ob[worst]:.3g}"
+    assert m["lse_violations"] == 0, f"{label}: LSE outside the bound (max err {m['lse_max_abs']:.3g})"
+    assert m["rel_l2"] <= 1e-2, f"{label}: rel L2 {m['rel_l2']:.3g} > 1e-2"
+    return m

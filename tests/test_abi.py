@@ -113,3 +113,26 @@ def test_fetch_dequant_validates(sm):
     assert L.snapmla_fetch_dequant(None, None, None, None, None, 2, 4, 4, 64, None, None) == 1    # null pointers
     assert L.snapmla_fetch_dequant(4104, 4096, 4096, 4096, 4096, 2, 4, 4, 64, 4096, None) == 4   # misaligned latent
     assert L.snapmla_fetch_dequant(4096, 4096, 4096, 4098, 4096, 2, 4, 4, 64, 4096, None) == 4   # misaligned table
+
+
+def test_bf16_entry_points_validate(sm):
+    L = sm.lib
+    # decode_bf16: same checks as snapmla_decode, no scale plane
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, None, 0,
+                                 None) == 2                                                     # page size
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 3, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+                                 None) == 1                                                     # q_len
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+                                 None) == 1                                                     # null pointers
+    assert L.snapmla_decode_bf16(4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096, 16,
+                                 None) == 3                                                     # workspace
+    assert L.snapmla_decode_bf16(4096, 4096, 4104, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096,
+                                 1 << 30, None) == 4                                            # misaligned cache
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+                                 None) == 0                                                     # B == 0
+    # append_bf16
+    assert L.snapmla_append_bf16(None, None, None, None, 1, 1, 4, 4, 32, None, None, None) == 2
+    assert L.snapmla_append_bf16(None, None, None, None, -1, 1, 4, 4, 64, None, None, None) == 1
+    assert L.snapmla_append_bf16(None, None, None, None, 0, 1, 4, 4, 64, None, None, None) == 0
+    assert L.snapmla_append_bf16(None, None, None, None, 2, 1, 4, 4, 64, None, None, None) == 1
+    assert L.snapmla_append_bf16(4096, 4096, 4096, 4096, 2, 1, 4, 4, 64, 4100, 4096, None) == 4
