@@ -41,7 +41,8 @@ def _log(msg):
 
 
 SOURCES_OF = {"decode": ("decode.hip", "quant.hip", "snapmla_device.h"),
-              "fetch_dequant": ("fetch.hip", "snapmla_device.h")}
+              "fetch_dequant": ("fetch.hip", "snapmla_device.h"),
+              "decode_bf16": ("decode_bf16.hip", "quant.hip", "snapmla_device.h")}
 
 
 def _src_hash(op="decode"):
@@ -206,6 +207,128 @@ def bench_fetch(args, w, run):
     print(json.dumps(line), flush=True)
 
 
+BF16_BYTES_PER_TOKEN = 2 * 512 + 2 * 64     # bf16 latent + bf16 rope
+
+
+def bf16_cpu_baseline(w, budget_s=15.0):
+    """The oracle's float64 attention on the bf16 inputs (mla.bf16_reference), on a bounded sample."""
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    from oracle import mla
+    qn, qr = w.queries()
+    el, toks, seqs = 0.0, 0, 0
+    for b in range(w.B):
+        N = int(w.seq_lens[b])
+        ck, kr = w.tokens(b, 0, N)
+        ts = time.perf_counter()
+        mla.bf16_reference(qn[b].reshape(-1, 512), qr[b].reshape(-1, 64), ck, kr, w.tau,
+                           mla.visible_counts(N, w.q_len, w.H, w.causal))
+        el += time.perf_counter() - ts
+        toks += N
+        seqs += 1
+        if el > budget_s and seqs >= 2:
+            break
+    return {"value": round(toks * BF16_BYTES_PER_TOKEN / el / 1e9, 3), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{seqs} of {w.B} sequences ({toks} KV tokens, {w.H * w.q_len} rows each): bf16_reference "
+                      f"in float64, {el:.1f} s"}
+
+
+def bench_bf16(args, w, run8):
+    """The BF16-cache step (append_bf16 + decode_bf16 + combine) on the same workload, timed beside the
+    FP8 step: the paper's FP8-vs-BF16 decode comparison on one MI355X."""
+    import numpy as np
+    import torch
+    from paper_2602_10718_amd.runner import DecodeRunner
+    t0 = time.perf_counter()
+    run16 = DecodeRunner(w, num_splits=run8.num_splits, out_dtype=torch.bfloat16, kv_dtype="bf16")
+    _log(f"bf16 cache filled in {time.perf_counter() - t0:.1f} s")
+    stream = torch.cuda.current_stream()
+
+    if args.traffic_probe:
+        src = torch.ones(1 << 26, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            run16.decode()
+            torch.cuda.synchronize()
+        print(json.dumps({"traffic_probe": True, "op": "decode_bf16", "copy_bytes_read": src.numel() * 4,
+                          "decode_calls": 3, "workload": w.name}), flush=True)
+        return
+
+    def timed(fn, k):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(k):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / k * 1e3
+
+    def per_call(run):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        for k in range(args.steps):
+            run.append()
+            ev[k][0].record(stream)
+            run.decode()
+            ev[k][1].record(stream)
+            run.combine()
+            ev[k][2].record(stream)
+        torch.cuda.synchronize()
+        return (float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3,
+                float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) * 1e3)
+
+    res = {}
+    for name, run in (("fp8", run8), ("bf16", run16)):
+        for _ in range(args.warmup):
+            run.step()
+        step_us = timed(run.step, args.steps)
+        dec_us, comb_us = per_call(run)
+        res[name] = {"step_us": round(step_us, 1), "decode_us": round(dec_us, 1), "combine_us": round(comb_us, 1)}
+        _log(f"{name}: step {step_us:.1f} us, decode {dec_us:.1f} us, combine {comb_us:.1f} us")
+    # interleaved repeat, so that a clock drift between the two legs does not decide the ratio
+    f8b = [timed(run8.step, args.steps) for _ in range(3)]
+    b16b = [timed(run16.step, args.steps) for _ in range(3)]
+    kv16 = w.total_tokens * BF16_BYTES_PER_TOKEN
+    kv8 = w.kv_bytes()
+    us16 = res["bf16"]["step_us"]
+    dec16 = res["bf16"]["decode_us"]
+    flops = 2.0 * w.total_tokens * 64 * ((w.H * w.q_len + 63) // 64) * (576 + 512)
+    gbps = kv16 / (us16 * 1e-6) / 1e9
+    dec_gbps = kv16 / (dec16 * 1e-6) / 1e9
+    line = {
+        "metric": "BF16-cache MLA decode µs/step + KV HBM GB/s beside the FP8 step, 64 heads, 8K-32K ctx",
+        "value": round(gbps, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(us16 * 1e-3, 4), "us_per_step": us16, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl_names()[args.config] + ", BF16 cache (1152 B per token)", "batch": w.B,
+                   "heads": w.H, "q_len": w.q_len, "kv_tokens": w.total_tokens, "kv_bytes_bf16": kv16,
+                   "kv_bytes_fp8": kv8, "num_splits": run16.num_splits,
+                   "step": "append_bf16 + decode_bf16 + combine"},
+        "fp8": res["fp8"], "bf16": res["bf16"],
+        "speedup_fp8_over_bf16": {"step": round(us16 / res["fp8"]["step_us"], 3),
+                                  "decode_call": round(dec16 / res["fp8"]["decode_us"], 3),
+                                  "step_repeats": [round(b / a, 3) for a, b in zip(f8b, b16b)],
+                                  "kv_byte_ratio": round(kv16 / kv8, 3)},
+        "roofline": {"bound": "hbm", "kernel": "snapmla_decode_bf16 call (prep_kernel + decode_bf16_kernel), "
+                                               "HIP events on its stream",
+                     "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": _traffic("bf16_" + w.name, "decode_bf16"),
+                     "algorithmic_bytes_per_launch": kv16,
+                     "mfma_frac_bf16": round(flops / (dec16 * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)},
+    }
+    if not args.no_cpu_baseline:
+        _log("cpu baseline (oracle bf16_reference) ...")
+        line["cpu_baseline"] = bf16_cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
 FP8_PEAK_TFLOPS = 5000.0       # dense FP8 MFMA
 BF16_PEAK_TFLOPS = 2500.0      # dense BF16 MFMA
 
@@ -366,11 +489,12 @@ def main():
     ap.add_argument("--num-splits", type=int, default=None)
     ap.add_argument("--cold-steps", type=int, default=20, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant", "sweep", "ablation"],
+    ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant", "sweep", "ablation", "decode_bf16"],
                     help="decode: the hot path step (default); fetch_dequant: snapmla_fetch_dequant over every "
                          "cached token of the workload; sweep: decode + combine for H in 16..128 x q_len in {1, 2} "
                          "at batch 32, lengths U[16K, 128K]; ablation: the cache quantized under each granularity "
-                         "of the accuracy ablation, decode error vs fp32 attention on the bf16 inputs")
+                         "of the accuracy ablation, decode error vs fp32 attention on the bf16 inputs; decode_bf16: the "
+                         "BF16-cache step on the same workload, timed beside the FP8 step")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: one 256 MiB device copy (counter calibration), then 3 "
                          "snapmla_decode calls; prints what it ran and exits")
@@ -402,6 +526,9 @@ def main():
 
     if args.op == "fetch_dequant":
         bench_fetch(args, w, run)
+        return
+    if args.op == "decode_bf16":
+        bench_bf16(args, w, run)
         return
 
     if args.traffic_probe:
