@@ -45,6 +45,10 @@ int check_shapes(int32_t B, int32_t q_len, int32_t H, int32_t num_splits, int32_
   if ((int64_t)q_len * H > 256)
     return fail(SNAPMLA_INVALID_ARGUMENT, "q_len*H must be <= 256 (got %d)", q_len * H);
   if (num_splits < 1) return fail(SNAPMLA_INVALID_ARGUMENT, "num_splits must be >= 1 (got %d)", num_splits);
+  if (kv_chunk_tokens > 0 && (int64_t)B * num_splits > (int64_t)1 << 26)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "B * num_splits must be <= 2^26 with fixed KV chunks (got %lld)",
+                (long long)B * num_splits);
+  if (num_splits > (1 << 26)) return fail(SNAPMLA_INVALID_ARGUMENT, "num_splits must be <= 2^26 (got %d)", num_splits);
   if (kv_chunk_tokens < 0 || kv_chunk_tokens % 64 != 0)
     return fail(SNAPMLA_INVALID_ARGUMENT, "kv_chunk_tokens must be 0 or a positive multiple of 64 (got %d)",
                 kv_chunk_tokens);
@@ -88,6 +92,8 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   p.prefix = reinterpret_cast<int32_t*>(ws + L.prefix);
   p.flags = reinterpret_cast<int32_t*>(ws + L.flags);
   p.zero = ws + L.zero;
+  p.desc = reinterpret_cast<int32_t*>(ws + L.desc);
+  p.units = L.units;
   p.B = B;
   p.q_len = q_len;
   p.max_pages = max_pages;
@@ -107,6 +113,7 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   d.page_table = page_table;
   d.seq_lens = seq_lens;
   d.prefix = p.prefix;
+  d.desc = p.desc;
   d.zero = p.zero;
   d.part_o = reinterpret_cast<float*>(ws + L.o);
   d.part_lse = reinterpret_cast<float*>(ws + L.lse);
@@ -145,6 +152,8 @@ WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens)
   L.prefix = off; off += align256(((size_t)B + 1) * 4);
   L.flags = off;  off += align256((size_t)B * 4);
   L.zero = off;   off += 1024;
+  L.units = kv_chunk_tokens == 0 ? num_splits : B * num_splits;   // <= 2^26 (check_shapes)
+  L.desc = off;   off += align256((size_t)L.units * kDescInts * 4);
   L.lse = off;    off += align256((size_t)L.pieces * L.rows_pad * 4);
   L.o = off;      off += align256((size_t)L.pieces * L.rows_pad * 512 * 4);
   L.total = off;

@@ -32,6 +32,8 @@
 // stored with the 16-byte chunk index XOR-swizzled by the token index (swz) so
 // that both the token-major QK reads and the transposed PV reads avoid bank
 // conflicts.  Page ids travel the same way, four blocks ahead of their copy.
+// A workgroup starts from the descriptor of its block range that the prep kernel
+// wrote (range and first sequence): no search of the split plan.
 //
 // Per block (matrices transposed so that one lane owns one query row):
 //   S^T[16 tok x 16 rows]  = K_c^T . q8^T   (16x16x128 FP8 MFMA, K = 512), 4 token tiles
@@ -91,16 +93,6 @@ constexpr int kSpinLimit = 1 << 22;
 __device__ __forceinline__ int swz(int t) { return (t & 15) ^ (((t >> 4) & 1) << 2); }
 __device__ __forceinline__ int rswz(int t) { return (t >> 1) & 7; }
 
-// Largest b with prefix[b] <= gb (prefix is non-decreasing, prefix[B] > gb).
-__device__ __forceinline__ int find_seq(const int32_t* __restrict__ prefix, int B, int gb) {
-  int lo = 0, hi = B - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (prefix[mid] <= gb) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
-
 // Handshake flags in LDS.  A wave's LDS operations complete in issue order, so
 // a flag stored after lds_wait_all() is seen only after the data stored before it.
 __device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
@@ -136,29 +128,22 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
   const int units = a.chunk_blocks == 0 ? a.num_splits : a.B * a.num_splits;
   if (unit >= units) return;
 
-  // ---- the global block range of this workgroup --------------------------
-  int gstart, gend;
-  if (a.chunk_blocks == 0) {
-    const int64_t T = prefix[a.B];
-    gstart = (int)((int64_t)unit * T / a.num_splits);
-    gend = (int)((int64_t)(unit + 1) * T / a.num_splits);
-  } else {
-    const int b = unit / a.num_splits, s = unit % a.num_splits;
-    const int nb = prefix[b + 1] - prefix[b];
-    const int k0 = s * a.chunk_blocks;
-    if (k0 >= nb) return;
-    gstart = prefix[b] + k0;
-    gend = prefix[b] + min(k0 + a.chunk_blocks, nb);
-  }
+  // ---- the global block range of this workgroup and its first piece, from the
+  // start descriptor the prep kernel wrote (one scalar load, no search) ------
+  const int32_t* dsc = a.desc + (int64_t)unit * kDescInts;
+  const int gstart = dsc[kDescStart], gend = dsc[kDescEnd];
   if (gstart >= gend) return;
   const int nblocks = gend - gstart;
 
-  // piece bookkeeping (identical in every wave; scalar)
-  int cur_b = -1, cur_blk0 = 0, cur_end = 0, cur_n = 0, cur_p0 = 0;
+  // piece bookkeeping (identical in every wave; scalar): the piece of the current
+  // block, and the next one, fetched a period before it starts
+  int cur_b = dsc[kDescSeq], cur_p0 = dsc[kDescP0], cur_end = dsc[kDescP1], cur_n = dsc[kDescLen];
+  int cur_blk0 = gstart - cur_p0;
+  int nx_b = 0, nx_p0 = 0, nx_end = 0, nx_n = 0;
   // (the three loads of the usual case, the next sequence, are issued together:
   // one memory round trip per piece; only sequences without blocks loop)
-  auto enter_piece = [&](int gb) {
-    int b = cur_b < 0 ? find_seq(prefix, a.B, gb) : cur_b + 1;
+  auto fetch_next = [&](int gb) {                 // gb: first block of the next piece
+    int b = cur_b + 1;
     int p0 = prefix[b], p1 = prefix[b + 1], nb = seq_lens[b];
     asm volatile("" ::"s"(nb));                   // keeps the length load beside the prefix loads
     while (p1 <= gb) {
@@ -167,11 +152,17 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       p1 = prefix[b + 1];
       nb = seq_lens[b];
     }
-    cur_b = b;
-    cur_p0 = p0;
-    cur_blk0 = gb - p0;
-    cur_end = p1;
-    cur_n = nb;
+    nx_b = b;
+    nx_p0 = p0;
+    nx_end = p1;
+    nx_n = nb;
+  };
+  auto take_next = [&](int gb) {
+    cur_b = nx_b;
+    cur_p0 = nx_p0;
+    cur_blk0 = gb - nx_p0;
+    cur_end = nx_end;
+    cur_n = nx_n;
   };
 
   if (is_qk && lane == 0) flag_store(xf + w, 0);   // ordered before any wait by the first barrier
@@ -204,32 +195,41 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     for (int s = 0; s < 2; ++s) roff[s] = (uint32_t)(n16 * (kDr * 2) + (((4 * s + g4) ^ (n16 >> 1)) << 4));
     const uint32_t soff = (uint32_t)(kRopeBytes + 16 * g4);
 
+    // queries and fresh row state of the current piece: for the first piece before
+    // the first barrier, for later ones right after the previous piece's last block
+    // was published, so the loads overlap the wait at the barrier
+    auto start_piece = [&]() {
+      vis = a.causal ? cur_n - a.q_len + 1 + row / a.H : cur_n;
+      if (row_ok) {
+        const int64_t qrow = (int64_t)cur_b * a.R + row;
+        const v4i* src = reinterpret_cast<const v4i*>(a.q8 + qrow * kDc);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const v4i lo4 = src[8 * s + 2 * g4], hi4 = src[8 * s + 2 * g4 + 1];
+          qv[s] = v8i{lo4[0], lo4[1], lo4[2], lo4[3], hi4[0], hi4[1], hi4[2], hi4[3]};
+        }
+        const v4i* rsrc = reinterpret_cast<const v4i*>(a.q_rope + qrow * kDr);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) qr[s] = rsrc[4 * s + g4];
+        cq = a.sq[qrow];
+      } else {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) qv[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < 2; ++s) qr[s] = v4i{0, 0, 0, 0};
+        cq = 0.f;
+      }
+      m = -INFINITY; sp = 1.0f; l = 0.0f;
+    };
+    start_piece();
+
     for (int k = 0; k < nblocks; ++k) {
       barrier_vm_lgkm0<63>();                              // page k has landed (PV waves waited)
       const int gb = gstart + k;
-      if (cur_b < 0 || gb >= cur_end) {                    // first block of a new piece
-        enter_piece(gb);
-        vis = a.causal ? cur_n - a.q_len + 1 + row / a.H : cur_n;
-        if (row_ok) {
-          const int64_t qrow = (int64_t)cur_b * a.R + row;
-          const v4i* src = reinterpret_cast<const v4i*>(a.q8 + qrow * kDc);
-#pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            const v4i lo4 = src[8 * s + 2 * g4], hi4 = src[8 * s + 2 * g4 + 1];
-            qv[s] = v8i{lo4[0], lo4[1], lo4[2], lo4[3], hi4[0], hi4[1], hi4[2], hi4[3]};
-          }
-          const v4i* rsrc = reinterpret_cast<const v4i*>(a.q_rope + qrow * kDr);
-#pragma unroll
-          for (int s = 0; s < 2; ++s) qr[s] = rsrc[4 * s + g4];
-          cq = a.sq[qrow];
-        } else {
-#pragma unroll
-          for (int s = 0; s < 4; ++s) qv[s] = v8i{0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-          for (int s = 0; s < 2; ++s) qr[s] = v4i{0, 0, 0, 0};
-          cq = 0.f;
-        }
-        m = -INFINITY; sp = 1.0f; l = 0.0f;
+      if (gb >= cur_end) {                                 // first block of a later piece
+        fetch_next(gb);
+        take_next(gb);
+        start_piece();
       }
       const int blk = gb - cur_p0;
       const uint8_t* st = smem + (k % kLatStages) * kLatBytes;             // latent of block k
@@ -359,8 +359,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     // page-table cursor (scalar): the next block asked for lies in sequence ib,
     // whose blocks are global blocks [ib_lo, ib_hi).  Blocks are asked for in
     // nondecreasing order; past the range the last block stands in.
-    int ib = find_seq(prefix, a.B, gstart);
-    int ib_lo = prefix[ib], ib_hi = prefix[ib + 1];
+    int ib = cur_b, ib_lo = cur_p0, ib_hi = cur_end;
     auto page_entry = [&](int kb) -> const int32_t* {
       const int gb = gstart + min(kb, nblocks - 1);
       while (gb >= ib_hi) {                        // skips sequences without blocks
@@ -543,7 +542,8 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       // ---- block k: piece bookkeeping (mirrors the QK waves) -----------------
       const int gb = gstart + k;
       if (gb >= cur_end) {
-        enter_piece(gb);
+        fetch_next(gb);
+        take_next(gb);
         cur_bad = false;
       }
       cur_bad |= ((stage_bad >> (k % kLatStages)) & 1u) != 0;

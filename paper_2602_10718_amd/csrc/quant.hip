@@ -82,16 +82,19 @@ __global__ __launch_bounds__(256) void encode_kernel(const float* __restrict__ x
 }
 
 // Query quantization (Fused-Q-Quant) over all rows, plus, in block 0, the split
-// plan: prefix[b] = number of 64-token blocks of valid sequences before b.
+// plan: prefix[b] = number of 64-token blocks of valid sequences before b, and the
+// start descriptor of every split unit (kDesc* layout).
 __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   if (blockIdx.x == 0) {
     __shared__ int sums[256];
+    __shared__ int lens[256];
     const int per = (a.B + 255) / 256;
     const int b0 = tid * per, b1 = min(a.B, b0 + per);
     int local = 0;
     for (int b = b0; b < b1; ++b) {
       const int n = a.seq_lens[b];
+      if (per == 1) lens[tid] = n;
       bool ok = (n == 0) || (n >= a.q_len && n <= a.max_pages * kPage);
       const int nb = (n + kPage - 1) / kPage;
       if (ok && a.chunk_blocks > 0) ok = (nb + a.chunk_blocks - 1) / a.chunk_blocks <= a.num_splits;
@@ -114,6 +117,44 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
       a.prefix[b + 1] = run;
     }
     reinterpret_cast<uint32_t*>(a.zero)[tid] = 0u;   // 256 threads x 4 B = 1 KiB
+    __syncthreads();                                 // prefix complete (LDS and global)
+
+    // ---- start descriptors, one unit per thread ----------------------------
+    // (with one sequence per thread, B <= 256, the scan's LDS sums are the prefix)
+    const int T = sums[255];
+    auto pref = [&](int i) { return per == 1 ? (i == 0 ? 0 : sums[i - 1]) : a.prefix[i]; };
+    for (int u = tid; u < a.units; u += 256) {
+      int32_t* d = a.desc + (int64_t)u * kDescInts;
+      int gs = 0, ge = 0, b = 0;
+      if (a.chunk_blocks == 0) {
+        gs = (int)((int64_t)u * T / a.num_splits);
+        ge = (int)((int64_t)(u + 1) * T / a.num_splits);
+        if (gs < ge) {                               // largest b with prefix[b] <= gs
+          int lo = 0, hi = a.B - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (pref(mid) <= gs) lo = mid; else hi = mid - 1;
+          }
+          b = lo;
+        }
+      } else {
+        b = u / a.num_splits;
+        const int64_t k0 = (int64_t)(u % a.num_splits) * a.chunk_blocks;
+        const int p0 = pref(b), nb = pref(b + 1) - p0;
+        if (k0 < nb) {
+          gs = p0 + (int)k0;
+          ge = p0 + (int)min<int64_t>(k0 + a.chunk_blocks, nb);
+        }
+      }
+      d[kDescStart] = gs;
+      d[kDescEnd] = ge;
+      if (gs >= ge) continue;
+      const int p0 = pref(b), p1 = pref(b + 1);
+      d[kDescSeq] = b;
+      d[kDescP0] = p0;
+      d[kDescP1] = p1;
+      d[kDescLen] = per == 1 ? lens[b] : a.seq_lens[b];
+    }
     return;
   }
   const int64_t nw = (int64_t)(gridDim.x - 1) * 4;

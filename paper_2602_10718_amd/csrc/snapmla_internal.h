@@ -10,7 +10,8 @@ namespace snapmla {
 // Workspace carve-up shared by decode and combine.
 struct WsLayout {
   int R = 0, G = 0, rows_pad = 0, pieces = 0;
-  size_t q8 = 0, sq = 0, prefix = 0, flags = 0, zero = 0, lse = 0, o = 0, total = 0;
+  int units = 0;
+  size_t q8 = 0, sq = 0, prefix = 0, flags = 0, zero = 0, desc = 0, lse = 0, o = 0, total = 0;
 };
 WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens);
 
@@ -23,8 +24,19 @@ struct PrepArgs {
   int32_t* prefix;          // [B+1] cumulative 64-token block counts of valid sequences
   int32_t* flags;           // [B] 1 = sequence rejected (data error)
   uint8_t* zero;            // 1 KiB that the decode kernel reads in place of slots past a sequence end
-  int B, q_len, max_pages, chunk_blocks, num_splits;
+  int32_t* desc;            // [units][kDescInts] start descriptor of each split unit (see kDesc*)
+  int B, q_len, max_pages, chunk_blocks, num_splits, units;
 };
+
+// Start descriptor of a split unit (a workgroup's range of 64-token blocks), written
+// by the prep kernel so that a workgroup begins without searching the plan:
+constexpr int kDescInts = 8;
+constexpr int kDescStart = 0;    // first global block of the range
+constexpr int kDescEnd = 1;      // one past the last (start >= end: nothing to do)
+constexpr int kDescSeq = 2;      // sequence of the first block
+constexpr int kDescP0 = 3;       // its first global block (prefix[seq])
+constexpr int kDescP1 = 4;       // one past its last (prefix[seq + 1])
+constexpr int kDescLen = 5;      // its length in tokens
 
 struct DecodeArgs {
   const uint16_t* q_nope;   // [B*R][512] bf16 (read by the BF16-cache kernel only)
@@ -37,6 +49,7 @@ struct DecodeArgs {
   const int32_t* page_table;
   const int32_t* seq_lens;
   const int32_t* prefix;
+  const int32_t* desc;      // [units][kDescInts]
   const uint8_t* zero;
   float* part_o;            // [pieces][rows_pad][512]
   float* part_lse;          // [pieces][rows_pad]
