@@ -34,6 +34,12 @@
 // conflicts.  Page ids travel the same way, four blocks ahead of their copy.
 // A workgroup starts from the descriptor of its block range that the prep kernel
 // wrote (range and first sequence): no search of the split plan.
+// Two PV-wave schedules (template flag kRotate, chosen by the launch): with one
+// row group, products of block k-1 first, then the copies, then the transposed
+// reads of block k into the same registers; with several row groups (pages shared
+// through L2, the period bound by the waves' own work), copies first, products,
+// then the transposed reads into a rotating set of six register slots, so that no
+// read waits for a product still reading its destination.
 //
 // Per block (matrices transposed so that one lane owns one query row):
 //   S^T[16 tok x 16 rows]  = K_c^T . q8^T   (16x16x128 FP8 MFMA, K = 512), 4 token tiles
@@ -95,7 +101,13 @@ __device__ __forceinline__ int rswz(int t) { return (t >> 1) & 7; }
 
 // Handshake flags in LDS.  A wave's LDS operations complete in issue order, so
 // a flag stored after lds_wait_all() is seen only after the data stored before it.
-__device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// (the builtin rather than inline asm: the compiler's own wait-count pass then
+// knows that every LDS result is in, and inserts no later waits for them)
+__device__ __forceinline__ void lds_wait_all() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);            // lgkmcnt(0); vmcnt and expcnt left alone
+  asm volatile("" ::: "memory");
+}
 __device__ __forceinline__ void flag_store(int* f, int v) {
   __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
@@ -107,6 +119,7 @@ __device__ __forceinline__ int flag_load(const int* f) {
 typedef __attribute__((address_space(3))) volatile v4i lds_flags4;
 __device__ __forceinline__ v4i flag_load4(const int* f) { return *(const lds_flags4*)(f); }
 
+template <bool kRotate>
 __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int32_t* __restrict__ prefix,
                                                         const int32_t* __restrict__ page_table,
                                                         const int32_t* __restrict__ seq_lens) {
@@ -453,139 +466,306 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       const int tok = 32 * (c & 1) + 16 * (tri >> 2) + 8 * h + 4 * (c >> 1) + (tri & 3);
       tr_off[c] = (uint32_t)(tok * kDc + 8 * trb) | (uint32_t)(((8 * dq + g16) ^ swz(tok)) << 4);
     }
-    // Top-of-period wait: block k (latent and RoPE) complete, and the page id
-    // read at the end of the period.  Loads complete in issue order: in steady
-    // state the RoPE copy of block k is followed by the latent copy of block k+1,
-    // the piece-end stores of period k-1 if any (kPieceStores of them) and its 12
-    // requests, so "at most 20 (+ kPieceStores) outstanding" suffices; 19 in
-    // period 0, after the prologue.
-    auto top_barrier = [&](int k, bool after_stores) {
-      if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
-      else if (k == 0) barrier_vm_lgkm0<19>();
-      else if (after_stores) barrier_vm_lgkm0<20 + kPieceStores>();
-      else barrier_vm_lgkm0<20>();
-    };
+    if constexpr (!kRotate) {
+      // Top-of-period wait: block k (latent and RoPE) complete, and the page id
+      // read at the end of the period.  Loads complete in issue order: in steady
+      // state the RoPE copy of block k is followed by the latent copy of block k+1,
+      // the piece-end stores of period k-1 if any (kPieceStores of them) and its 12
+      // requests, so "at most 20 (+ kPieceStores) outstanding" suffices; 19 in
+      // period 0, after the prologue.
+      auto top_barrier = [&](int k, bool after_stores) {
+        if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
+        else if (k == 0) barrier_vm_lgkm0<19>();
+        else if (after_stores) barrier_vm_lgkm0<20 + kPieceStores>();
+        else barrier_vm_lgkm0<20>();
+      };
 
-    v2i rv[4][4];                 // V^T tiles of the pending block
-    v8i P0, P1;                   // its codes, row tiles 0 and 1
-    v4f gl0, gl1;                 // its per-row state {gamma, l, m, sigma_P}
-    bool cur_bad = false;
-    bool stored = false;          // the previous period wrote piece results
-    for (int k = 0;; ++k) {
-      top_barrier(k, stored);
-      stored = false;
-      if (k > 0) {
-        // ---- PV of block k-1 --------------------------------------------------
-#pragma unroll
+      v2i rv[4][4];                 // V^T tiles of the pending block
+      v8i P0, P1;                   // its codes, row tiles 0 and 1
+      v4f gl0, gl1;                 // its per-row state {gamma, l, m, sigma_P}
+      bool cur_bad = false;
+      bool stored = false;          // the previous period wrote piece results
+      for (int k = 0;; ++k) {
+        top_barrier(k, stored);
+        stored = false;
+        if (k > 0) {
+          // ---- PV of block k-1 --------------------------------------------------
+  #pragma unroll
+          for (int T = 0; T < 4; ++T) {
+            O[2 * T] *= gl0[0];
+            O[2 * T + 1] *= gl1[0];
+          }
+  #pragma unroll
+          for (int T = 0; T < 4; ++T) {
+            const v8i A = v8i{rv[T][0][0], rv[T][0][1], rv[T][1][0], rv[T][1][1],
+                              rv[T][2][0], rv[T][2][1], rv[T][3][0], rv[T][3][1]};
+            O[2 * T] = mfma_f8_32x32x64(A, P0, O[2 * T]);
+            O[2 * T + 1] = mfma_f8_32x32x64(A, P1, O[2 * T + 1]);
+          }
+          // ---- end of a piece: write the normalized partial output and LSE ----
+          // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
+          if (k == nblocks || gstart + k >= cur_end) {
+            const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
+                                                    : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
+            const float nanv = __builtin_nanf("");
+            // Exactly kPieceStores store instructions per wave, whatever R: rows up to
+            // rows_pad lie inside the piece's slot (the combine reads rows < R only),
+            // and every wave writes the same LSE values.  The next top-of-period wait
+            // counts them.
+  #pragma unroll
+            for (int r = 0; r < 2; ++r) {
+              const int row = r == 0 ? row0 : row1;
+              const v4f gl = r == 0 ? gl0 : gl1;
+              const float lfin = gl[1];
+              const bool empty = !(lfin > 0.0f);
+              float inv = empty ? 0.0f : 1.0f / lfin;
+              if (cur_bad) inv = nanv;
+              float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
+  #pragma unroll
+              for (int T = 0; T < 4; ++T) {
+  #pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                  *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
+                      v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
+                          O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
+                  __builtin_amdgcn_sched_barrier(0);
+                }
+              }
+              if (h == 0) {
+                float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
+                if (cur_bad) lse = nanv;
+                a.part_lse[pid * a.rows_pad + row] = lse;
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
+  #pragma unroll
+            for (int T = 0; T < 8; ++T) O[T] = v16f{0};
+            stored = true;
+          }
+        }
+        // copies after the products and the piece-end stores, so that the stores
+        // precede the period's copies in the wait counter
+        if (k + 2 < nblocks) {
+          request_page(k + 6);
+          copy_rope_scale(k + 2, pg_rope);
+          copy_latent(k + 3, pg_lat);
+          pg_rope = pg_lat;
+        }
+        if (k == nblocks) break;
+
+        // ---- block k: piece bookkeeping (mirrors the QK waves) -----------------
+        const int gb = gstart + k;
+        if (gb >= cur_end) {
+          fetch_next(gb);
+          take_next(gb);
+          cur_bad = false;
+        }
+        cur_bad |= ((stage_bad >> (k % kLatStages)) & 1u) != 0;
+        const int valid = min(kPage, cur_n - (gb - cur_p0) * kPage);
+        uint8_t* stp = smem + (k % kLatStages) * kLatBytes;
+        if (valid < kPage) {
+          // last page of a sequence: clear the bytes of the slots past its end that
+          // this wave reads (stale data could hold NaN codes; their probability
+          // codes are 0).  The QK waves mask these slots whatever they hold.
+          const int nz = (kPage - valid) * 8;
+          for (int i = lane; i < nz; i += 64) {
+            const int t = valid + (i >> 3);
+            const int c = 8 * dq + (i & 7);
+            *reinterpret_cast<v4i*>(stp + t * kDc + ((c ^ swz(t)) << 4)) = v4i{0, 0, 0, 0};
+          }
+        }
+        // V^T tiles of block k
+        const uint32_t st_lds = smem_base + (k % kLatStages) * kLatBytes;
+  #pragma unroll
         for (int T = 0; T < 4; ++T) {
+  #pragma unroll
+          for (int c = 0; c < 4; ++c) rv[T][c] = lds_read_tr8_at((st_lds | tr_off[c]) ^ (uint32_t)(T << 5));
+        }
+        // codes and state of block k, once all four QK waves have published them
+        for (int spin = 0; spin < kSpinLimit; ++spin) {
+          const v4i f4 = flag_load4(xf);
+          if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
+        }
+        asm volatile("" ::: "memory");
+        gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
+        gl1 = *reinterpret_cast<const v4f*>(xg + (n + 32) * 4);
+        // B operand of row tile r: bytes 32h .. 32h+31 of row 32r + n (the K order
+        // of the PV product, see the transposed reads)
+        const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h);
+        const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h + 16);
+        const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h);
+        const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h + 16);
+        P0 = v8i{c00[0], c00[1], c00[2], c00[3], c01[0], c01[1], c01[2], c01[3]};
+        P1 = v8i{c10[0], c10[1], c10[2], c10[3], c11[0], c11[1], c11[2], c11[3]};
+        const int pg_next = pg_ring_p[(k + 4) & 3];   // id of block k+4 (stale when not copied)
+        lds_wait_all();
+        pg_lat = __builtin_amdgcn_readfirstlane(pg_next);
+      }
+    } else {
+      // Top-of-period wait: block k (latent and RoPE) complete, and the page id
+      // read at the end of the period.  Loads complete in issue order.  Each period
+      // issues its 12 requests first and the piece-end stores, if any, after them, so
+      // in steady state the RoPE copy of block k (period k-2) is followed by the
+      // latent copy of block k+1, the stores of period k-2, the 12 requests of period
+      // k-1 and its stores: "at most 20 (+ kPieceStores per storing period)
+      // outstanding" suffices (capped at the counter's range, which only waits
+      // longer); 19 in period 0, after the prologue.
+      auto top_barrier = [&](int k, int storing_periods) {
+        if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
+        else if (k == 0) barrier_vm_lgkm0<19>();
+        else if (storing_periods == 0) barrier_vm_lgkm0<20>();
+        else if (storing_periods == 1) barrier_vm_lgkm0<20 + kPieceStores>();
+        else barrier_vm_lgkm0<63>();
+      };
+
+      // V^T tiles in six 8-register slots: tile T of block k-1 sits in old[T]; the
+      // transposed reads of block k, issued after the products of block k-1, go to
+      // two free slots (tiles 0, 1) and to the slots of tiles 0 and 1 of block k-1
+      // (tiles 2, 3).  So no read waits for a product still reading its destination,
+      // and the slot roles rotate with period 3.
+      v2i sA[4], sB[4], sC[4], sD[4], sE[4], sF[4];
+      v8i P0, P1;                   // codes of the pending block, row tiles 0 and 1
+      v4f gl0, gl1;                 // its per-row state {gamma, l, m, sigma_P}
+      bool cur_bad = false;
+      bool st1 = false, st2 = false;   // periods k-1 and k-2 wrote piece results
+      auto period = [&](int k, v2i (&o0)[4], v2i (&o1)[4], v2i (&o2)[4], v2i (&o3)[4], v2i (&f0)[4],
+                        v2i (&f1)[4]) -> bool {
+        const bool PV = k > 0, RD = k < nblocks;   // products of block k-1, reads of block k
+        top_barrier(k, (st1 ? 1 : 0) + (st2 ? 1 : 0));
+        st2 = st1;
+        st1 = false;
+        if (k + 2 < nblocks) {
+          request_page(k + 6);
+          copy_rope_scale(k + 2, pg_rope);
+          copy_latent(k + 3, pg_lat);
+          pg_rope = pg_lat;
+        }
+        // the piece that block k-1 closes, if any (before the bookkeeping of block k)
+        const bool close = PV && (!RD || gstart + k >= cur_end);
+        const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
+                                                : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
+        const bool close_bad = cur_bad;
+        if (RD) {
+          // ---- block k: piece bookkeeping (mirrors the QK waves) ---------------
+          const int gb = gstart + k;
+          if (gb >= cur_end) {
+            fetch_next(gb);
+            take_next(gb);
+            cur_bad = false;
+          }
+          cur_bad |= ((stage_bad >> (k % kLatStages)) & 1u) != 0;
+          const int valid = min(kPage, cur_n - (gb - cur_p0) * kPage);
+          uint8_t* stp = smem + (k % kLatStages) * kLatBytes;
+          if (valid < kPage) {
+            // last page of a sequence: clear the bytes of the slots past its end that
+            // this wave reads (stale data could hold NaN codes; their probability
+            // codes are 0).  The QK waves mask these slots whatever they hold.
+            const int nz = (kPage - valid) * 8;
+            for (int i = lane; i < nz; i += 64) {
+              const int t = valid + (i >> 3);
+              const int c = 8 * dq + (i & 7);
+              *reinterpret_cast<v4i*>(stp + t * kDc + ((c ^ swz(t)) << 4)) = v4i{0, 0, 0, 0};
+            }
+          }
+        }
+        // ---- PV of block k-1, then the V^T reads of block k ---------------------
+        const uint32_t st_lds = smem_base + (k % kLatStages) * kLatBytes;
+        auto pv_tile = [&](int T, v2i (&src)[4]) {
           O[2 * T] *= gl0[0];
           O[2 * T + 1] *= gl1[0];
-        }
-#pragma unroll
-        for (int T = 0; T < 4; ++T) {
-          const v8i A = v8i{rv[T][0][0], rv[T][0][1], rv[T][1][0], rv[T][1][1],
-                            rv[T][2][0], rv[T][2][1], rv[T][3][0], rv[T][3][1]};
+          const v8i A = v8i{src[0][0], src[0][1], src[1][0], src[1][1], src[2][0], src[2][1], src[3][0], src[3][1]};
           O[2 * T] = mfma_f8_32x32x64(A, P0, O[2 * T]);
           O[2 * T + 1] = mfma_f8_32x32x64(A, P1, O[2 * T + 1]);
+        };
+        auto tr_tile = [&](int T, v2i (&dst)[4]) {
+  #pragma unroll
+          for (int c = 0; c < 4; ++c) dst[c] = lds_read_tr8_at((st_lds | tr_off[c]) ^ (uint32_t)(T << 5));
+        };
+        // all products first, then all reads: tiles 0 and 1 of block k go to the free
+        // slots, tiles 2 and 3 to the slots of tiles 0 and 1 of block k-1, whose
+        // products are done by the time the later products have been issued
+        if (PV) {
+          pv_tile(0, o0);
+          pv_tile(1, o1);
+          pv_tile(2, o2);
+          pv_tile(3, o3);
         }
-        // ---- end of a piece: write the normalized partial output and LSE ----
-        // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
-        if (k == nblocks || gstart + k >= cur_end) {
-          const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
-                                                  : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
-          const float nanv = __builtin_nanf("");
-          // Exactly kPieceStores store instructions per wave, whatever R: rows up to
-          // rows_pad lie inside the piece's slot (the combine reads rows < R only),
-          // and every wave writes the same LSE values.  The next top-of-period wait
-          // counts them.
-#pragma unroll
-          for (int r = 0; r < 2; ++r) {
-            const int row = r == 0 ? row0 : row1;
-            const v4f gl = r == 0 ? gl0 : gl1;
-            const float lfin = gl[1];
-            const bool empty = !(lfin > 0.0f);
-            float inv = empty ? 0.0f : 1.0f / lfin;
-            if (cur_bad) inv = nanv;
-            float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
-#pragma unroll
-            for (int T = 0; T < 4; ++T) {
-#pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
-                    v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
-                        O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
-                __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (RD) {
+          tr_tile(0, f0);
+          tr_tile(1, f1);
+          tr_tile(2, o0);
+          tr_tile(3, o1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (PV) {
+          // ---- end of a piece: write the normalized partial output and LSE --
+          // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
+          if (close) {
+            const float nanv = __builtin_nanf("");
+            // Exactly kPieceStores store instructions per wave, whatever R: rows up to
+            // rows_pad lie inside the piece's slot (the combine reads rows < R only),
+            // and every wave writes the same LSE values.  The next top-of-period
+            // waits count them.
+  #pragma unroll
+            for (int r = 0; r < 2; ++r) {
+              const int row = r == 0 ? row0 : row1;
+              const v4f gl = r == 0 ? gl0 : gl1;
+              const float lfin = gl[1];
+              const bool empty = !(lfin > 0.0f);
+              float inv = empty ? 0.0f : 1.0f / lfin;
+              if (close_bad) inv = nanv;
+              float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
+  #pragma unroll
+              for (int T = 0; T < 4; ++T) {
+  #pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                  *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
+                      v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
+                          O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
+                  __builtin_amdgcn_sched_barrier(0);
+                }
               }
+              if (h == 0) {
+                float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
+                if (close_bad) lse = nanv;
+                a.part_lse[pid * a.rows_pad + row] = lse;
+              }
+              __builtin_amdgcn_sched_barrier(0);
             }
-            if (h == 0) {
-              float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
-              if (cur_bad) lse = nanv;
-              a.part_lse[pid * a.rows_pad + row] = lse;
-            }
-            __builtin_amdgcn_sched_barrier(0);
+  #pragma unroll
+            for (int T = 0; T < 8; ++T) O[T] = v16f{0};
+            st1 = true;
           }
-#pragma unroll
-          for (int T = 0; T < 8; ++T) O[T] = v16f{0};
-          stored = true;
         }
-      }
-      // copies after the products and the piece-end stores, so that the stores
-      // precede the period's copies in the wait counter
-      if (k + 2 < nblocks) {
-        request_page(k + 6);
-        copy_rope_scale(k + 2, pg_rope);
-        copy_latent(k + 3, pg_lat);
-        pg_rope = pg_lat;
-      }
-      if (k == nblocks) break;
-
-      // ---- block k: piece bookkeeping (mirrors the QK waves) -----------------
-      const int gb = gstart + k;
-      if (gb >= cur_end) {
-        fetch_next(gb);
-        take_next(gb);
-        cur_bad = false;
-      }
-      cur_bad |= ((stage_bad >> (k % kLatStages)) & 1u) != 0;
-      const int valid = min(kPage, cur_n - (gb - cur_p0) * kPage);
-      uint8_t* stp = smem + (k % kLatStages) * kLatBytes;
-      if (valid < kPage) {
-        // last page of a sequence: clear the bytes of the slots past its end that
-        // this wave reads (stale data could hold NaN codes; their probability
-        // codes are 0).  The QK waves mask these slots whatever they hold.
-        const int nz = (kPage - valid) * 8;
-        for (int i = lane; i < nz; i += 64) {
-          const int t = valid + (i >> 3);
-          const int c = 8 * dq + (i & 7);
-          *reinterpret_cast<v4i*>(stp + t * kDc + ((c ^ swz(t)) << 4)) = v4i{0, 0, 0, 0};
+        if (!RD) return false;
+        // codes and state of block k, once all four QK waves have published them
+        for (int spin = 0; spin < kSpinLimit; ++spin) {
+          const v4i f4 = flag_load4(xf);
+          if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
         }
+        asm volatile("" ::: "memory");
+        gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
+        gl1 = *reinterpret_cast<const v4f*>(xg + (n + 32) * 4);
+        // B operand of row tile r: bytes 32h .. 32h+31 of row 32r + n (the K order
+        // of the PV product, see the transposed reads)
+        const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h);
+        const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h + 16);
+        const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h);
+        const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h + 16);
+        P0 = v8i{c00[0], c00[1], c00[2], c00[3], c01[0], c01[1], c01[2], c01[3]};
+        P1 = v8i{c10[0], c10[1], c10[2], c10[3], c11[0], c11[1], c11[2], c11[3]};
+        const int pg_next = pg_ring_p[(k + 4) & 3];   // id of block k+4 (stale when not copied)
+        lds_wait_all();
+        pg_lat = __builtin_amdgcn_readfirstlane(pg_next);
+        return true;
+      };
+      // three periods per iteration: the slot roles rotate without register copies
+      for (int k = 0;; k += 3) {
+        if (!period(k, sA, sB, sC, sD, sE, sF)) break;        // block k   -> E F A B
+        if (!period(k + 1, sE, sF, sA, sB, sC, sD)) break;    // block k+1 -> C D E F
+        if (!period(k + 2, sC, sD, sE, sF, sA, sB)) break;    // block k+2 -> A B C D
       }
-      // V^T tiles of block k
-      const uint32_t st_lds = smem_base + (k % kLatStages) * kLatBytes;
-#pragma unroll
-      for (int T = 0; T < 4; ++T) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) rv[T][c] = lds_read_tr8_at((st_lds | tr_off[c]) ^ (uint32_t)(T << 5));
-      }
-      // codes and state of block k, once all four QK waves have published them
-      for (int spin = 0; spin < kSpinLimit; ++spin) {
-        const v4i f4 = flag_load4(xf);
-        if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
-      }
-      asm volatile("" ::: "memory");
-      gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
-      gl1 = *reinterpret_cast<const v4f*>(xg + (n + 32) * 4);
-      // B operand of row tile r: bytes 32h .. 32h+31 of row 32r + n (the K order
-      // of the PV product, see the transposed reads)
-      const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h);
-      const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h + 16);
-      const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h);
-      const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h + 16);
-      P0 = v8i{c00[0], c00[1], c00[2], c00[3], c01[0], c01[1], c01[2], c01[3]};
-      P1 = v8i{c10[0], c10[1], c10[2], c10[3], c11[0], c11[1], c11[2], c11[3]};
-      const int pg_next = pg_ring_p[(k + 4) & 3];   // id of block k+4 (stale when not copied)
-      lds_wait_all();
-      pg_lat = __builtin_amdgcn_readfirstlane(pg_next);
     }
   }
 }
@@ -595,8 +775,16 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
   if (units <= 0) return hipSuccess;
   const int64_t grid = (int64_t)((units + 7) / 8) * 8 * a.G;
   if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(decode_kernel, dim3((unsigned)grid), dim3(64 * kWaves), 0, stream, a, a.prefix, a.page_table,
-                     a.seq_lens);
+  // With several row groups the workgroups of a unit share its pages through L2 and
+  // the period is bound by the waves' own work: there the copies go first and the
+  // products of block k-1 precede the transposed reads of block k (kRotate).  With
+  // one row group the pages come from HBM and the products go first.
+  if (a.G > 1)
+    hipLaunchKernelGGL(decode_kernel<true>, dim3((unsigned)grid), dim3(64 * kWaves), 0, stream, a, a.prefix,
+                       a.page_table, a.seq_lens);
+  else
+    hipLaunchKernelGGL(decode_kernel<false>, dim3((unsigned)grid), dim3(64 * kWaves), 0, stream, a, a.prefix,
+                       a.page_table, a.seq_lens);
   return hipGetLastError();
 }
 
