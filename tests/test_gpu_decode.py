@@ -128,3 +128,23 @@ def test_bf16_output():
     r32 = _run(w, num_splits=8)
     r16 = _run(w, num_splits=8, out_dtype=torch.bfloat16)
     assert torch.equal(r32.out.to(torch.bfloat16).view(torch.int16), r16.out.view(torch.int16))
+
+
+def test_plan_with_many_sequences_and_units():
+    """Split plans whose start descriptors take the prep kernel's general paths: more
+    sequences than scan threads (B = 300, the prefix read back from global memory) and
+    more units than threads (fixed chunks: 300 sequences x 2 chunks)."""
+    rng = np.random.default_rng(36)
+    lens = rng.integers(1, 260, 300).astype(np.int32)
+    lens[[5, 77, 150]] = 0                                  # empty sequences inside the range
+    w = wl.custom(B=300, H=16, q_len=1, seq_lens=lens.tolist(), seed=36)
+    qn, qr = w.queries()
+    for kw in (dict(num_splits=40), dict(num_splits=2, kv_chunk_tokens=192)):
+        run = _run(w, **kw)
+        out = run.out.cpu().numpy()
+        assert np.all(np.isfinite(out)), f"{kw}: non-finite output"
+        lse = run.lse.cpu().numpy()
+        for b in (5, 77, 150):                              # empty: output 0, LSE -inf
+            assert np.all(out[b] == 0) and np.all(lse[b] == -np.inf)
+        for b in (0, 1, 4, 6, 76, 78, 149, 151, 255, 256, 257, 299):
+            check_sequence(run, b, reference(w, b, qn, qr), label=f"many-seq {kw}")
