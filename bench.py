@@ -10,8 +10,9 @@ Default workload: 64-head MLA decode, batch 64, one query token, ragged context
 lengths uniform in [8192, 32768], 64-token pages in shuffled physical order.
 
 `value` is the achieved KV-cache read rate, sum of context lengths x 644 B per
-token / step time, over K back-to-back steps.  Also reported: the same step
-captured once as a HIP graph and replayed, cold-cache step times (a 1 GiB
+token / step time, over K back-to-back steps after W warm-up steps.  Also
+reported: the same step captured once as a HIP graph and replayed (no faster
+here: the eager launches overlap their gaps), cold-cache step times (a 1 GiB
 scratch write and read between steps, outside the timed region: the read
 leaves the caches clean, so no write-back of scratch lines lands inside the
 step), the per-call split, the roofline of the decode call and the CPU oracle
@@ -484,7 +485,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--config", type=int, default=3, help="workload 1..5 (3 is the headline)")
     ap.add_argument("--num-splits", type=int, default=None)
     ap.add_argument("--cold-steps", type=int, default=20, help="cold-cache steps (0 to skip)")
@@ -556,6 +557,9 @@ def main():
         return a.elapsed_time(b) / k
 
     # ---- warm-up, then the timed region: K back-to-back steps ---------------
+    # (the warm-up is long enough, ~0.2 s at the default, for the GPU's clocks to
+    # settle under this load: after 20 steps the first timed steps still ran ~9 %
+    # slower than after 1,000)
     for _ in range(args.warmup):
         run.step()
     torch.cuda.synchronize()
@@ -566,7 +570,7 @@ def main():
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         run.step()
-    for _ in range(args.warmup):
+    for _ in range(20):
         graph.replay()
     graph_us = timed(graph.replay, args.steps) * 1e3
     _log(f"graph replay: {graph_us:.1f} us/step")
