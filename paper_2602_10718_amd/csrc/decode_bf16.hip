@@ -53,15 +53,6 @@ constexpr float kLn2f = 0.69314718055994531f;
 // in 8 distinct groups.  RoPE rows (128 B): chunk c at c ^ ((t >> 1) & 7).
 __device__ __forceinline__ int swz(int t) { return ((t & 3) << 1) | ((t >> 2) & 1) | (t & 8); }
 
-__device__ __forceinline__ int find_seq_h(const int32_t* __restrict__ prefix, int B, int gb) {
-  int lo = 0, hi = B - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (prefix[mid] <= gb) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
-
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 __device__ __forceinline__ void fstore(int* f, int v) {
   __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -102,26 +93,17 @@ __global__ __launch_bounds__(512, 1) void decode_bf16_kernel(DecodeArgs a, const
   const int units = a.chunk_blocks == 0 ? a.num_splits : a.B * a.num_splits;
   if (unit >= units) return;
 
-  // the 64-token block range of this workgroup (same plan as the FP8 path)
-  int gstart, gend;
-  if (a.chunk_blocks == 0) {
-    const int64_t T = prefix[a.B];
-    gstart = (int)((int64_t)unit * T / a.num_splits);
-    gend = (int)((int64_t)(unit + 1) * T / a.num_splits);
-  } else {
-    const int b = unit / a.num_splits, s = unit % a.num_splits;
-    const int nb = prefix[b + 1] - prefix[b];
-    const int k0 = s * a.chunk_blocks;
-    if (k0 >= nb) return;
-    gstart = prefix[b] + k0;
-    gend = prefix[b] + min(k0 + a.chunk_blocks, nb);
-  }
+  // the 64-token block range of this workgroup and its first piece, from the start
+  // descriptor the prep kernel wrote (same plan as the FP8 path)
+  const int32_t* dsc = a.desc + (int64_t)unit * kDescInts;
+  const int gstart = dsc[kDescStart], gend = dsc[kDescEnd];
   if (gstart >= gend) return;
   const int nblk = 2 * (gend - gstart);            // 32-token blocks: two per 64-token block
 
-  int cur_b = -1, cur_blk0 = 0, cur_end = 0, cur_n = 0, cur_p0 = 0;
-  auto enter_piece = [&](int gb) {
-    int b = cur_b < 0 ? find_seq_h(prefix, a.B, gb) : cur_b + 1;
+  int cur_b = dsc[kDescSeq], cur_p0 = dsc[kDescP0], cur_end = dsc[kDescP1], cur_n = dsc[kDescLen];
+  int cur_blk0 = gstart - cur_p0;
+  auto enter_piece = [&](int gb) {                 // a later piece: sequence cur_b + 1 onwards
+    int b = cur_b + 1;
     int p0 = prefix[b], p1 = prefix[b + 1], nb = seq_lens[b];
     asm volatile("" ::"s"(nb));
     while (p1 <= gb) {
@@ -159,11 +141,13 @@ __global__ __launch_bounds__(512, 1) void decode_bf16_kernel(DecodeArgs a, const
 #pragma unroll
     for (int s = 0; s < 2; ++s) roff[s] = (uint32_t)(n16 * (kDr * 2) + (((4 * s + g4) ^ (n16 >> 1)) << 4));
 
+    bool fresh = true;                              // the first piece comes from the descriptor
     for (int k = 0; k < nblk; ++k) {
       barrier_vm_lgkm0<63>();
       const int gb = gstart + (k >> 1), hk = k & 1;
-      if (cur_b < 0 || gb >= cur_end) {
-        enter_piece(gb);
+      if (fresh || gb >= cur_end) {
+        if (!fresh) enter_piece(gb);
+        fresh = false;
         vis = a.causal ? cur_n - a.q_len + 1 + row / a.H : cur_n;
         if (row_ok) {
           const int64_t qrow = (int64_t)cur_b * a.R + row;
@@ -252,8 +236,7 @@ __global__ __launch_bounds__(512, 1) void decode_bf16_kernel(DecodeArgs a, const
     const int rtok = 8 * dq + (lane >> 3);
     const uint32_t rope_v = (uint32_t)((lane >> 3) * (kDr * 2) + (((lane & 7) ^ ((rtok >> 1) & 7)) << 4));
 
-    int ib = find_seq_h(prefix, a.B, gstart);
-    int ib_lo = prefix[ib], ib_hi = prefix[ib + 1];
+    int ib = cur_b, ib_lo = cur_p0, ib_hi = cur_end;
     auto page_entry = [&](int kb) -> const int32_t* {
       const int gb = gstart + min(kb >> 1, (nblk >> 1) - 1);
       while (gb >= ib_hi) {
