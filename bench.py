@@ -488,7 +488,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--config", type=int, default=3, help="workload 1..5 (3 is the headline)")
     ap.add_argument("--num-splits", type=int, default=None)
-    ap.add_argument("--cold-steps", type=int, default=20, help="cold-cache steps (0 to skip)")
+    ap.add_argument("--cold-steps", type=int, default=50, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant", "sweep", "ablation", "decode_bf16"],
                     help="decode: the hot path step (default); fetch_dequant: snapmla_fetch_dequant over every "
@@ -586,6 +586,7 @@ def main():
         run.combine()
         ev[k][3].record(stream)
     torch.cuda.synchronize()
+    step_each = np.array([e[0].elapsed_time(e[3]) for e in ev]) * 1e3
     append_us = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
     decode_us = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) * 1e3
     combine_us = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
@@ -641,6 +642,8 @@ def main():
         "us_per_step_graph": round(graph_us, 1),
         "breakdown_us": {"append": round(append_us, 2), "decode": round(decode_us, 2),
                          "combine": round(combine_us, 2)},
+        "warm_step_us_each": {"steps": args.steps, "median": round(float(np.median(step_each)), 1),
+                              "p90": round(float(np.percentile(step_each, 90)), 1)},
         "cold_cache": cold,
         "roofline": {
             "bound": "hbm",

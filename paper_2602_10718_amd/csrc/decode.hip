@@ -74,7 +74,9 @@ constexpr int kRsStages = 3;
 constexpr int kRsBase = kLatStages * kLatBytes;   // LDS offset of the RoPE/scale ring
 constexpr int kXBase = kRsBase + kRsStages * kRsBytes;
 constexpr int kWaves = 8;
-constexpr int kXcBytes = 64 * 64;               // probability codes [row][64 token slots]
+constexpr int kXcBytes = 64 * 64;               // probability codes [row][64 token slots]; 16-byte
+                                                // chunk c of row r at chunk c ^ ((r >> 2) & 3), so that
+                                                // 16 consecutive rows hit 16 distinct bank groups
 constexpr int kXgBytes = 2 * 32 * 16;           // per-row gamma, l, m, sigma_p [rt][row] x float4
 constexpr int kXfBytes = 4 * 4;                 // handshake flags of the QK waves
 constexpr int kXpBytes = 4 * 4 * 4;             // page-id ring of the PV waves [wave][4 slots]
@@ -343,9 +345,10 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           mine[t] = wd;
         }
       }
-      // codes of tokens 16t + 4g4 + v at byte 16 g4 + 4t + v of the row; the PV
+      // codes of tokens 16t + 4g4 + v at byte 16 g4 + 4t + v of the row (logical; the
+      // 16-byte chunk g4 sits at chunk g4 ^ ((row >> 2) & 3)); the PV
       // waves read the previous block's before this period's barrier
-      *reinterpret_cast<v4i*>(xc + (16 * w + n16) * 64 + 16 * g4) = mine;
+      *reinterpret_cast<v4i*>(xc + (16 * w + n16) * 64 + 16 * (g4 ^ ((n16 >> 2) & 3))) = mine;
       if (g4 == 0) *reinterpret_cast<v4f*>(xg + (16 * w + n16) * 4) = v4f{gam, l, m, sp};
       lds_wait_all();
       if (lane == 0) flag_store(xf + w, k + 1);   // block k published
@@ -591,10 +594,11 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         gl1 = *reinterpret_cast<const v4f*>(xg + (n + 32) * 4);
         // B operand of row tile r: bytes 32h .. 32h+31 of row 32r + n (the K order
         // of the PV product, see the transposed reads)
-        const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h);
-        const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h + 16);
-        const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h);
-        const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h + 16);
+        const int cs = (n >> 2) & 3;                  // chunk swizzle of rows n and 32 + n
+        const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 16 * ((2 * h) ^ cs));
+        const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 16 * ((2 * h + 1) ^ cs));
+        const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 16 * ((2 * h) ^ cs));
+        const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 16 * ((2 * h + 1) ^ cs));
         P0 = v8i{c00[0], c00[1], c00[2], c00[3], c01[0], c01[1], c01[2], c01[3]};
         P1 = v8i{c10[0], c10[1], c10[2], c10[3], c11[0], c11[1], c11[2], c11[3]};
         const int pg_next = pg_ring_p[(k + 4) & 3];   // id of block k+4 (stale when not copied)
@@ -749,10 +753,11 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         gl1 = *reinterpret_cast<const v4f*>(xg + (n + 32) * 4);
         // B operand of row tile r: bytes 32h .. 32h+31 of row 32r + n (the K order
         // of the PV product, see the transposed reads)
-        const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h);
-        const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 32 * h + 16);
-        const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h);
-        const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 32 * h + 16);
+        const int cs = (n >> 2) & 3;                  // chunk swizzle of rows n and 32 + n
+        const v4i c00 = *reinterpret_cast<const v4i*>(xc + n * 64 + 16 * ((2 * h) ^ cs));
+        const v4i c01 = *reinterpret_cast<const v4i*>(xc + n * 64 + 16 * ((2 * h + 1) ^ cs));
+        const v4i c10 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 16 * ((2 * h) ^ cs));
+        const v4i c11 = *reinterpret_cast<const v4i*>(xc + (32 + n) * 64 + 16 * ((2 * h + 1) ^ cs));
         P0 = v8i{c00[0], c00[1], c00[2], c00[3], c01[0], c01[1], c01[2], c01[3]};
         P1 = v8i{c10[0], c10[1], c10[2], c10[3], c11[0], c11[1], c11[2], c11[3]};
         const int pg_next = pg_ring_p[(k + 4) & 3];   // id of block k+4 (stale when not copied)
