@@ -194,7 +194,7 @@ def bench_fetch(args, w, run):
         "value": round(gbps, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4), "us_per_step": round(ms * 1e3, 1), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "e4m3->bf16", "data": "synthetic",
-        "config": {"workload": wl_names()[args.config] + " cache, every token fetched", "tokens": int(cu[-1]),
+        "config": {"workload": wl_describe(args.workload) + " cache, every token fetched", "tokens": int(cu[-1]),
                    "sequences": w.B, "bytes_per_call": nbytes, "step": "snapmla_fetch_dequant"},
         "roofline": {"bound": "hbm", "kernel": "fetch_dequant_kernel, HIP events on its stream",
                      "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -308,7 +308,7 @@ def bench_bf16(args, w, run8):
         "value": round(gbps, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(us16 * 1e-3, 4), "us_per_step": us16, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl_names()[args.config] + ", BF16 cache (1152 B per token)", "batch": w.B,
+        "config": {"workload": wl_describe(args.workload) + ", BF16 cache (1152 B per token)", "batch": w.B,
                    "heads": w.H, "q_len": w.q_len, "kv_tokens": w.total_tokens, "kv_bytes_bf16": kv16,
                    "kv_bytes_fp8": kv8, "num_splits": run16.num_splits,
                    "step": "append_bf16 + decode_bf16 + combine"},
@@ -476,9 +476,9 @@ def bench_ablation(args):
     print(json.dumps(line), flush=True)
 
 
-def wl_names():
+def wl_describe(name):
     from paper_2602_10718_amd import workloads as wl
-    return wl.CONFIG_NAMES
+    return wl.describe(name)
 
 
 def main():
@@ -486,7 +486,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=1000)
-    ap.add_argument("--config", type=int, default=3, help="workload 1..5 (3 is the headline)")
+    ap.add_argument("--workload", default="headline",
+                    choices=("tiny", "dsv3", "headline", "longsplit", "mtp"), help="workload by name")
     ap.add_argument("--num-splits", type=int, default=None)
     ap.add_argument("--cold-steps", type=int, default=50, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -502,7 +503,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the decode path shards by "
-              "sequence / head / KV chunk without collectives; see DESIGN.md)", file=sys.stderr)
+              "sequence / head / KV chunk without collectives)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -517,7 +518,7 @@ def main():
     if args.op == "ablation":
         bench_ablation(args)
         return
-    w = wl.make(args.config)
+    w = wl.make(args.workload)
     t_fill = time.perf_counter()
     run = DecodeRunner(w, num_splits=args.num_splits, out_dtype=torch.bfloat16)
     t_fill = time.perf_counter() - t_fill
@@ -632,7 +633,7 @@ def main():
         "dtype": "e4m3",
         "data": "synthetic",
         "config": {
-            "workload": wl.CONFIG_NAMES[args.config],
+            "workload": wl.describe(args.workload),
             "batch": w.B, "heads": w.H, "q_len": w.q_len, "causal": bool(w.causal),
             "ctx_min": int(w.seq_lens.min()), "ctx_max": int(w.seq_lens.max()),
             "kv_tokens": w.total_tokens, "kv_bytes": kv_bytes, "page": 64,

@@ -15,7 +15,7 @@ D is the E4M3 decoding (``e4m3.decode``); the product of a 4-significant-bit
 value and a float32 scale is exact in float64, so forming it in float64 and
 rounding once to float32 equals the float32 product; bf16() rounds to nearest,
 ties to even.  Readings (the paper gives the operator's purpose, not its
-rounding or layout; each is listed in the design doc): the output keeps the
+rounding or layout; these choices are ours): the output keeps the
 per-token row layout of the cache (latent then RoPE), the latent is rounded
 to bf16 once from the float32 product, NaN becomes the canonical 0x7FC0.
 Data errors: a token whose page id lies outside [0, num_pages), and every

@@ -15,7 +15,7 @@ per-token quantizer (``quant.quantize_rows``):
     C        per-tensor dynamic: one scale over every content value of the batch
     D        per-block: one scale per 64-token block (page) of a sequence
 
-Readings (the table names the granularities only; each is listed in the design doc):
+Readings (the table names the granularities only; these choices are ours):
 the "tensor" of C is the cache of the whole batch; the blocks of D are the
 64-token pages, aligned to position 0; in A the RoPE part shares the token's
 scale and the decode path reads it back as bf16(fp32(sigma * D(code))).

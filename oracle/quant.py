@@ -12,7 +12,7 @@ division).  For one row x of bf16 values:
     y_i   = fp32(x_i / sigma)                   (IEEE float32 division, RNE)
     code_i = E4M3(y_i)                          (RNE, satfinite)
 
-Readings (the paper does not fix these; each is listed in the design doc):
+Readings (the paper does not fix these; these choices are ours):
   * the per-token scale is amax/448, the same rule Algorithm 1 uses for the
     probability blocks;
   * the quotient is formed in float32 and then rounded to E4M3 -- two

@@ -148,42 +148,48 @@ def _finish(w):
     return w
 
 
-CONFIG_NAMES = {
-    1: "tiny B1 H16 ctx256",
-    2: "dsv3-shaped B32 H128 ctx4096",
-    3: "64-head ragged 8K-32K B64",
-    4: "long split B8 H64 ctx128K x32 chunks",
-    5: "MTP B128 H128 q_len2 causal ragged 1K-16K",
+# The five workloads, by name: what each is, and the seed its inputs come from.
+WORKLOADS = {
+    "tiny": ("tiny B1 H16 ctx256", 1001),
+    "dsv3": ("dsv3-shaped B32 H128 ctx4096", 1002),
+    "headline": ("64-head ragged 8K-32K B64", 1003),
+    "longsplit": ("long split B8 H64 ctx128K x32 chunks", 1004),
+    "mtp": ("MTP B128 H128 q_len2 causal ragged 1K-16K", 1005),
 }
 
 
-def make(cfg, seed=None, B=None, ctx=None, ctx_range=None):
-    """Build workload `cfg` (1..5).  B / ctx / ctx_range shrink it for fast tests."""
-    seed = 1000 + cfg if seed is None else seed
+def describe(name):
+    """One-line description of workload `name`."""
+    return WORKLOADS[name][0]
+
+
+def make(name, seed=None, B=None, ctx=None, ctx_range=None):
+    """Build workload `name` (a key of WORKLOADS).  B / ctx / ctx_range shrink it for fast tests."""
+    if name not in WORKLOADS:
+        raise ValueError(f"unknown workload {name!r}; one of {sorted(WORKLOADS)}")
+    seed = WORKLOADS[name][1] if seed is None else seed
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0])))
-    if cfg == 1:
+    if name == "tiny":
         b = B or 1
         w = Workload("tiny", b, 16, 1, False, np.full(b, ctx or 256, np.int32), 1, 1.0, False, seed,
                      shuffle_pages=False)
-    elif cfg == 2:
+    elif name == "dsv3":
         b = B or 32
         w = Workload("dsv3", b, 128, 1, False, np.full(b, ctx or 4096, np.int32), 1, 1.0, False, seed)
-    elif cfg == 3:
+    elif name == "headline":
         b = B or 64
         lo, hi = ctx_range or (8192, 32768)
         w = Workload("headline", b, 64, 1, False, rng.integers(lo, hi + 1, b).astype(np.int32), 1, 1.5,
                      True, seed)
-    elif cfg == 4:
+    elif name == "longsplit":
         b = B or 8
         w = Workload("longsplit", b, 64, 1, False, np.full(b, ctx or 131072, np.int32), 1, 1.0, False, seed,
                      kv_chunk_tokens=4096)
-    elif cfg == 5:
+    else:   # "mtp"
         b = B or 128
         lo, hi = ctx_range or (1024, 16384)
         w = Workload("mtp", b, 128, 2, True, rng.integers(lo, hi + 1, b).astype(np.int32), 2, 1.0, False,
                      seed)
-    else:
-        raise ValueError(f"unknown workload {cfg}")
     return _finish(w)
 
 

@@ -19,7 +19,7 @@ def _run(w, **kw):
 
 
 CASES = {
-    "tiny-cfg1": (lambda: wl.make(1), dict(num_splits=8)),
+    "tiny": (lambda: wl.make("tiny"), dict(num_splits=8)),
     "ragged-h16": (lambda: wl.custom(B=4, H=16, q_len=1, seq_lens=[1, 31, 33, 517], seed=41), dict(num_splits=16)),
     "ragged-h64-rotary": (lambda: wl.custom(B=3, H=64, q_len=1, seq_lens=[700, 129, 1000], sigma_tok=1.5,
                                             rotary=True, seed=42), dict(num_splits=24)),
@@ -117,15 +117,15 @@ def test_bf16_and_fp8_paths_differ_as_the_oracle_predicts():
     assert abs(rel - rel_oracle) <= 0.02 * rel_oracle
 
 
-@pytest.mark.parametrize("cfg,nsample", [(3, 3)])
-def test_full_size_sampled_parity_bf16(cfg, nsample):
-    w = wl.make(cfg)
+@pytest.mark.parametrize("name,nsample", [("headline", 3)])
+def test_full_size_sampled_parity_bf16(name, nsample):
+    w = wl.make(name)
     run = runner(w, kv_dtype="bf16")
-    print(f"[cfg{cfg} bf16] B={w.B} H={w.H} tokens={w.total_tokens} splits={run.num_splits}", flush=True)
+    print(f"[{name} bf16] B={w.B} H={w.H} tokens={w.total_tokens} splits={run.num_splits}", flush=True)
     run.step()
     torch.cuda.synchronize()
     out = run.out.cpu().numpy()
     assert np.all(np.isfinite(out)) and np.all(np.isfinite(run.lse.cpu().numpy()))
     qn, qr = w.queries()
     for b in sorted(set(int(round(x)) for x in np.linspace(0, w.B - 1, nsample))):
-        check_sequence_bf16(run, b, reference_bf16(w, b, qn, qr), label=f"cfg{cfg}-bf16")
+        check_sequence_bf16(run, b, reference_bf16(w, b, qn, qr), label=f"{name}-bf16")

@@ -21,7 +21,7 @@ def _run(w, **kw):
 
 CASES = {
     # name: (workload factory, runner kwargs)
-    "tiny-cfg1": (lambda: wl.make(1), dict(num_splits=8)),
+    "tiny": (lambda: wl.make("tiny"), dict(num_splits=8)),
     "ragged-h16": (lambda: wl.custom(B=4, H=16, q_len=1, seq_lens=[1, 63, 64, 517], seed=21), dict(num_splits=16)),
     "ragged-h64-rotary": (lambda: wl.custom(B=3, H=64, q_len=1, seq_lens=[700, 129, 1000], sigma_tok=1.5,
                                             rotary=True, seed=22), dict(num_splits=24)),

@@ -132,7 +132,7 @@ def test_cache_written_by_append():
 
 def test_headline_cache_sampled():
     """The bench launch: every sequence of the headline cache, sampled sequences checked bit for bit."""
-    w = wl.make(3)
+    w = wl.make("headline")
     from paper_2602_10718_amd.runner import DecodeRunner
     run = DecodeRunner(w)
     cu = _cu(w.seq_lens)

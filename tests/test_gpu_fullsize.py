@@ -26,20 +26,20 @@ def _sample(B, n):
     return sorted(set(int(round(x)) for x in np.linspace(0, B - 1, n)))
 
 
-@pytest.mark.parametrize("cfg,nsample", [(2, 3), (3, 3), (4, 2), (5, 8)])
-def test_full_size_sampled_parity(cfg, nsample):
-    w = wl.make(cfg)
+@pytest.mark.parametrize("name,nsample", [("dsv3", 3), ("headline", 3), ("longsplit", 2), ("mtp", 8)])
+def test_full_size_sampled_parity(name, nsample):
+    w = wl.make(name)
     run = runner(w, out_dtype=torch.float32)
-    print(f"[cfg{cfg}] B={w.B} H={w.H} q_len={w.q_len} tokens={w.total_tokens} splits={run.num_splits} "
+    print(f"[{name}] B={w.B} H={w.H} q_len={w.q_len} tokens={w.total_tokens} splits={run.num_splits} "
           f"chunk={run.kv_chunk_tokens}", flush=True)
     run.step()
     torch.cuda.synchronize()
     out = run.out.cpu().numpy()
     lse = run.lse.cpu().numpy()
-    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse)), f"cfg{cfg}: non-finite output"
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse)), f"{name}: non-finite output"
     qn, qr = w.queries()
     for b in _sample(w.B, nsample):
-        check_sequence(run, b, reference(w, b, qn, qr), label=f"cfg{cfg}")
+        check_sequence(run, b, reference(w, b, qn, qr), label=name)
     # the tokens appended by the step landed bit-exactly in their pages
     for b in _sample(w.B, 4):
         N = int(w.seq_lens[b])
@@ -47,6 +47,6 @@ def test_full_size_sampled_parity(cfg, nsample):
         ck, kr = w.tokens(b, lo, N)
         codes, scales = quant.quantize_rows(ck)
         c_dev, s_dev, r_dev = run.sequence_cache(b)
-        assert np.array_equal(c_dev[lo:N], codes), f"cfg{cfg} b={b}: appended codes differ"
-        assert np.array_equal(s_dev[lo:N].view(np.uint32), scales.view(np.uint32)), f"cfg{cfg} b={b}: scales"
-        assert np.array_equal(r_dev[lo:N], kr), f"cfg{cfg} b={b}: rope bits"
+        assert np.array_equal(c_dev[lo:N], codes), f"{name} b={b}: appended codes differ"
+        assert np.array_equal(s_dev[lo:N].view(np.uint32), scales.view(np.uint32)), f"{name} b={b}: scales"
+        assert np.array_equal(r_dev[lo:N], kr), f"{name} b={b}: rope bits"
