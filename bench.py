@@ -476,6 +476,33 @@ def bench_ablation(args):
     print(json.dumps(line), flush=True)
 
 
+def read_ceiling(run, w, timed, units=256, reps=50):
+    """Time snapmla_debug_read_ceiling over the decode's pages: every 64-token block of every
+    sequence in order, streamed into LDS with the decode's copy structure and no attention
+    arithmetic, one workgroup per CU as in the decode launch.  Returns its time, its rate in
+    bytes of whole pages (41,216 B per block), and the ceiling's time over the decode call's
+    (decode_call_frac, filled in by the caller)."""
+    import numpy as np
+    import torch
+    from paper_2602_10718_amd import snapmla as sm
+    npg = (w.seq_lens.astype(np.int64) + 63) // 64
+    pages = np.concatenate([w.page_table[b, :npg[b]] for b in range(w.B)]).astype(np.int32)
+    pages_d = torch.from_numpy(pages).cuda()
+    units = max(units, -(-len(pages) // 1792))
+    out = torch.empty(units, dtype=torch.int32, device="cuda")
+
+    def call():
+        sm.snapmla_debug_read_ceiling(run.kv_latent, run.kv_scale, run.k_rope, pages_d, run.kv_latent.shape[0],
+                                      units, out)
+    for _ in range(20):
+        call()
+    ms = timed(call, reps)
+    page_bytes = len(pages) * 41216
+    return {"kernel": "read_ceiling_kernel (snapmla_debug_read_ceiling), HIP events", "units": units,
+            "blocks": len(pages), "us": round(ms * 1e3, 1), "page_bytes": page_bytes,
+            "GBps": round(page_bytes / (ms * 1e-3) / 1e9, 1)}
+
+
 def wl_describe(name):
     from paper_2602_10718_amd import workloads as wl
     return wl.describe(name)
@@ -614,8 +641,13 @@ def main():
                 "median_GBps": round(kv_bytes / (float(np.median(ts)) * 1e-6) / 1e9, 1)}
         _log(f"cold: median {cold['median_us']} us, p90 {cold['p90_us']} us")
 
+    # ---- read-stream ceiling over the same pages (a measurement kernel) --------
+    ceiling = read_ceiling(run, w, timed)
+    _log(f"read-stream ceiling: {ceiling['us']} us, {ceiling['GBps']} GB/s of whole pages")
+
     gbps = kv_bytes / (ms_per_step * 1e-3) / 1e9
     decode_gbps = kv_bytes / (decode_us * 1e-6) / 1e9
+    ceiling["decode_call_frac"] = round(ceiling["us"] / decode_us, 4)
     traffic = _traffic(w.name, "decode")
     line = {
         "metric": METRIC,
@@ -655,6 +687,7 @@ def main():
             "frac": round(decode_gbps / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": kv_bytes,
+            "read_ceiling": ceiling,
         },
         "cache_fill_s": round(t_fill, 1),
     }

@@ -271,6 +271,27 @@ int snapmla_quantize_cache_config(const void* c_kv, const void* k_rope, const in
  */
 int snapmla_e4m3_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t stream);
 
+/*
+ * snapmla_debug_read_ceiling -- measurement hook, not part of the attention
+ * path: streams the cache pages of nblk 64-token blocks into LDS with the same
+ * direct-to-LDS copy structure and ring depth as snapmla_decode (latent three
+ * blocks ahead, RoPE and scales two), without any attention arithmetic.  Its
+ * duration is the read-stream ceiling of that page stream, against which the
+ * decode's bandwidth is reported.
+ *   kv_latent, kv_scale, k_rope   cache planes (device, read; 16-byte aligned)
+ *   pages   int32 [nblk]  physical page of each block in stream order (device,
+ *           read); ids outside [0, num_pages) read page 0
+ *   units   workgroups; unit u streams blocks [u*nblk/units, (u+1)*nblk/units),
+ *           at most 1792 of them (SNAPMLA_INVALID_ARGUMENT otherwise)
+ *   out     uint32 [units] (device, written): per unit, the XOR over its blocks
+ *           of the first 256 dwords of the latent page and of the RoPE page
+ *           (each dword XORed with its counterpart), folded over the 256
+ *           dword positions, so a test can check that every page was read
+ */
+int snapmla_debug_read_ceiling(const uint8_t* kv_latent, const float* kv_scale, const void* k_rope,
+                               const int32_t* pages, int32_t nblk, int32_t num_pages, int32_t units,
+                               uint32_t* out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -342,3 +342,29 @@ int snapmla_quantize_cache_config(const void* c_kv, const void* k_rope, const in
 }
 
 }  // extern "C"
+
+int snapmla_debug_read_ceiling(const uint8_t* kv_latent, const float* kv_scale, const void* k_rope,
+                               const int32_t* pages, int32_t nblk, int32_t num_pages, int32_t units,
+                               uint32_t* out, hipStream_t stream) {
+  if (nblk < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "nblk must be >= 0 (got %d)", nblk);
+  if (units < 1 || units > (1 << 20)) return fail(SNAPMLA_INVALID_ARGUMENT, "units must be in [1, 2^20] (got %d)", units);
+  if (num_pages < 1) return fail(SNAPMLA_INVALID_ARGUMENT, "num_pages must be >= 1 (got %d)", num_pages);
+  if (((int64_t)nblk + units - 1) / units > snapmla::kCeilingMaxBlocks)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "at most %d blocks per unit: use units >= %lld", snapmla::kCeilingMaxBlocks,
+                (long long)(((int64_t)nblk + snapmla::kCeilingMaxBlocks - 1) / snapmla::kCeilingMaxBlocks));
+  if (!out || (nblk > 0 && (!kv_latent || !kv_scale || !k_rope || !pages)))
+    return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer");
+  if (misaligned(kv_latent) || misaligned(kv_scale) || misaligned(k_rope))
+    return fail(SNAPMLA_MISALIGNED, "kv_latent, kv_scale and k_rope must be 16-byte aligned");
+  if (misaligned4(pages) || misaligned4(out)) return fail(SNAPMLA_MISALIGNED, "pages and out must be 4-byte aligned");
+  snapmla::CeilingArgs a;
+  a.kv_latent = kv_latent;
+  a.kv_scale = kv_scale;
+  a.k_rope = static_cast<const uint16_t*>(k_rope);
+  a.pages = pages;
+  a.out = out;
+  a.nblk = nblk;
+  a.num_pages = num_pages;
+  a.units = units;
+  return hip_status(snapmla::launch_read_ceiling(a, stream), "read_ceiling launch");
+}

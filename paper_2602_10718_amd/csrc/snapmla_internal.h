@@ -98,4 +98,16 @@ hipError_t launch_quantize_cache_config(const uint16_t* c_kv, const uint16_t* k_
                                         uint32_t* amax_word, uint8_t* kv_latent, float* kv_scale,
                                         uint16_t* k_rope_out, hipStream_t stream);
 
+// Read-stream ceiling (measurement): the pages of nblk blocks streamed into LDS.
+constexpr int kCeilingMaxBlocks = 1792;   // blocks per workgroup (their page ids sit in LDS)
+struct CeilingArgs {
+  const uint8_t* kv_latent;
+  const float* kv_scale;
+  const uint16_t* k_rope;
+  const int32_t* pages;     // [nblk] physical page of each block, in stream order
+  uint32_t* out;            // [units] per-workgroup checksum
+  int nblk, num_pages, units;
+};
+hipError_t launch_read_ceiling(const CeilingArgs& a, hipStream_t stream);
+
 }  // namespace snapmla

@@ -57,10 +57,13 @@ lib.snapmla_append_bf16.restype = ctypes.c_int
 lib.snapmla_append_bf16.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p]
 lib.snapmla_fetch_dequant.restype = ctypes.c_int
 lib.snapmla_fetch_dequant.argtypes = [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]
+lib.snapmla_debug_read_ceiling.restype = ctypes.c_int
+lib.snapmla_debug_read_ceiling.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p]
 
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
-           "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16"]
+           "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16",
+           "snapmla_debug_read_ceiling"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -113,6 +116,14 @@ def snapmla_quantize_append(c_kv_new, k_rope_new, page_table, seq_lens, num_page
 def snapmla_quantize_rows(x, codes, scale, stream=None):
     """x bf16 [rows, 512] -> codes uint8 [rows, 512], scale f32 [rows]."""
     _check(lib.snapmla_quantize_rows(_ptr(x), x.numel() // 512, _ptr(codes), _ptr(scale), _stream(stream)))
+
+
+def snapmla_debug_read_ceiling(kv_latent, kv_scale, k_rope, pages, num_pages, units, out, stream=None):
+    """Measurement hook: stream the cache pages listed in `pages` (int32 [nblk], stream order) into LDS
+    through the decode's copy structure, with no attention arithmetic; `out` uint32-sized int32 [units]
+    receives per-unit checksums (XOR of the first KiB of every latent and RoPE page of the unit)."""
+    _check(lib.snapmla_debug_read_ceiling(_ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope), _ptr(pages), pages.numel(),
+                                          num_pages, units, _ptr(out), _stream(stream)))
 
 
 def snapmla_e4m3_encode(x, codes, stream=None):

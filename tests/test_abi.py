@@ -136,3 +136,15 @@ def test_bf16_entry_points_validate(sm):
     assert L.snapmla_append_bf16(None, None, None, None, 0, 1, 4, 4, 64, None, None, None) == 0
     assert L.snapmla_append_bf16(None, None, None, None, 2, 1, 4, 4, 64, None, None, None) == 1
     assert L.snapmla_append_bf16(4096, 4096, 4096, 4096, 2, 1, 4, 4, 64, 4100, 4096, None) == 4
+
+
+def test_read_ceiling_validates(sm):
+    L = sm.lib
+    assert L.snapmla_debug_read_ceiling(None, None, None, None, -1, 4, 1, None, None) == 1        # nblk < 0
+    assert L.snapmla_debug_read_ceiling(None, None, None, None, 10, 4, 0, None, None) == 1        # units < 1
+    assert L.snapmla_debug_read_ceiling(None, None, None, None, 10, 0, 1, None, None) == 1        # num_pages < 1
+    assert L.snapmla_debug_read_ceiling(4096, 4096, 4096, 4096, 1793, 4, 1, 4096, None) == 1      # > 1792 per unit
+    assert L.snapmla_debug_read_ceiling(None, None, None, None, 10, 4, 1, 4096, None) == 1        # null pointers
+    assert L.snapmla_debug_read_ceiling(4104, 4096, 4096, 4096, 10, 4, 1, 4096, None) == 4        # misaligned plane
+    assert L.snapmla_debug_read_ceiling(4096, 4096, 4096, 4098, 10, 4, 1, 4096, None) == 4        # misaligned pages
+
