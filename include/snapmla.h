@@ -164,6 +164,31 @@ int snapmla_decode(const void* q_nope, const void* q_rope,
                    hipStream_t stream);
 
 /*
+ * snapmla_append_decode -- snapmla_quantize_append of the step's n_new tokens
+ * per sequence followed by snapmla_decode, with the quantize-on-append run in
+ * the same preparation launch as the query quantization (Section 3.3, Layer 1
+ * fuses both token preparations ahead of the attention kernel).  The result,
+ * the cache bytes written and the error behaviour are those of the two calls in
+ * sequence on `stream`; one kernel launch fewer.
+ *   c_kv_new bf16 [B][n_new][512], k_rope_new bf16 [B][n_new][64]   device, read;
+ *            token t of sequence b goes to position seq_lens[b] - n_new + t
+ *            (n_new == 0: no append, the pointers may be NULL)
+ *   kv_latent, kv_scale, k_rope   cache planes, written at the new tokens' slots
+ *            and then read by the decode
+ *   every other argument as snapmla_decode
+ */
+int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t n_new,
+                          const void* q_nope, const void* q_rope,
+                          uint8_t* kv_latent, float* kv_scale, void* k_rope,
+                          const int32_t* page_table, const int32_t* seq_lens,
+                          int32_t B, int32_t q_len, int32_t H,
+                          int32_t max_pages, int32_t num_pages, int32_t page_size,
+                          float softmax_scale, int32_t causal,
+                          int32_t num_splits, int32_t kv_chunk_tokens,
+                          void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
+/*
  * snapmla_decode_bf16 -- the BF16-cache baseline of the paper's comparison
  * (Section 4: the FP8 kernel against MLA decode over a BF16 cache).  Same
  * queries, page table, split plan, workspace and combine as snapmla_decode; the

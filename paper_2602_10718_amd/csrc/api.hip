@@ -57,11 +57,20 @@ int check_shapes(int32_t B, int32_t q_len, int32_t H, int32_t num_splits, int32_
 
 // snapmla_decode and snapmla_decode_bf16: validation, workspace carve-up, the prep
 // launch (query quantization only for the FP8 cache) and the decode launch.
+// New tokens that snapmla_append_decode quantizes and appends inside the decode's
+// preparation launch (n_new == 0: none).
+struct AppendIn {
+  const void* c_kv_new = nullptr;
+  const void* k_rope_new = nullptr;
+  int32_t n_new = 0;
+};
+
 int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent, const float* kv_scale,
                   const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
                   int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
                   float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
-                  void* workspace, size_t workspace_bytes, hipStream_t stream, bool bf16_cache) {
+                  void* workspace, size_t workspace_bytes, hipStream_t stream, bool bf16_cache,
+                  const AppendIn& app = AppendIn()) {
   int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
   if (st != SNAPMLA_OK) return st;
   if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
@@ -81,6 +90,13 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
     return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
   if (workspace_bytes < L.total)
     return fail(SNAPMLA_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes (got %zu)", L.total, workspace_bytes);
+  const int64_t app_toks = (int64_t)B * app.n_new;
+  if (app_toks > 0) {
+    if (!app.c_kv_new || !app.k_rope_new) return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+    if (misaligned(app.c_kv_new) || misaligned(app.k_rope_new))
+      return fail(SNAPMLA_MISALIGNED, "c_kv_new and k_rope_new must be 16-byte aligned");
+    if ((app_toks + 3) / 4 > 0x3FFFFFFF) return fail(SNAPMLA_INVALID_ARGUMENT, "too many new tokens");
+  }
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   snapmla::PrepArgs p;
@@ -99,6 +115,17 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   p.max_pages = max_pages;
   p.chunk_blocks = kv_chunk_tokens / 64;
   p.num_splits = num_splits;
+  if (app_toks > 0) {
+    p.c_kv_new = static_cast<const uint16_t*>(app.c_kv_new);
+    p.k_rope_new = static_cast<const uint16_t*>(app.k_rope_new);
+    p.page_table = page_table;
+    p.kv_latent = static_cast<uint8_t*>(const_cast<void*>(kv_latent));
+    p.kv_scale = const_cast<float*>(kv_scale);
+    p.k_rope = static_cast<uint16_t*>(const_cast<void*>(k_rope));
+    p.n_new = app.n_new;
+    p.num_pages = num_pages;
+    p.ablocks = (int)((app_toks + 3) / 4);
+  }
   hipError_t e = snapmla::launch_prep(p, stream);
   if (e != hipSuccess) return hip_status(e, "decode prep launch");
 
@@ -224,6 +251,22 @@ int snapmla_decode(const void* q_nope, const void* q_rope, const uint8_t* kv_lat
   return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
                        num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
                        workspace_bytes, stream, false);
+}
+
+int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t n_new, const void* q_nope,
+                          const void* q_rope, uint8_t* kv_latent, float* kv_scale, void* k_rope,
+                          const int32_t* page_table, const int32_t* seq_lens, int32_t B, int32_t q_len, int32_t H,
+                          int32_t max_pages, int32_t num_pages, int32_t page_size, float softmax_scale,
+                          int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream) {
+  if (n_new < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "n_new must be >= 0 (got %d)", n_new);
+  AppendIn app;
+  app.c_kv_new = c_kv_new;
+  app.k_rope_new = k_rope_new;
+  app.n_new = n_new;
+  return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
+                       num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
+                       workspace_bytes, stream, false, app);
 }
 
 int snapmla_decode_bf16(const void* q_nope, const void* q_rope, const void* kv_latent, const void* k_rope,

@@ -46,17 +46,16 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(const uint16_t* __re
     quantize_row_wave(x + r * kDc, codes + r * kDc, scale + r, lane);
 }
 
-// Fused-K-Append (Section 3.3, Layer 1): quantize each new token and write it,
-// with its unscaled bf16 RoPE row and its scale, into its paged slot.
-__global__ __launch_bounds__(256) void append_kernel(const uint16_t* __restrict__ c_kv_new,
-                                                     const uint16_t* __restrict__ k_rope_new,
-                                                     const int32_t* __restrict__ page_table,
-                                                     const int32_t* __restrict__ seq_lens, int B, int n_new,
-                                                     int max_pages, int num_pages, uint8_t* __restrict__ kv_latent,
-                                                     float* __restrict__ kv_scale, uint16_t* __restrict__ k_rope) {
-  const int lane = threadIdx.x & 63;
-  const int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (tok >= (int64_t)B * n_new) return;
+// Fused-K-Append (Section 3.3, Layer 1): quantize new token `tok` (token t of
+// sequence b, tok = b*n_new + t) and write it, with its unscaled bf16 RoPE row
+// and its scale, into its paged slot.  One wave per token.
+__device__ __forceinline__ void append_token_wave(const uint16_t* __restrict__ c_kv_new,
+                                                  const uint16_t* __restrict__ k_rope_new,
+                                                  const int32_t* __restrict__ page_table,
+                                                  const int32_t* __restrict__ seq_lens, int64_t tok, int n_new,
+                                                  int max_pages, int num_pages, uint8_t* __restrict__ kv_latent,
+                                                  float* __restrict__ kv_scale, uint16_t* __restrict__ k_rope,
+                                                  int lane) {
   const int b = (int)(tok / n_new), t = (int)(tok % n_new);
   const int pos = seq_lens[b] - n_new + t;
   if (pos < 0 || pos >= max_pages * kPage) return;
@@ -66,6 +65,19 @@ __global__ __launch_bounds__(256) void append_kernel(const uint16_t* __restrict_
   quantize_row_wave(c_kv_new + tok * kDc, kv_latent + slot * kDc, kv_scale + slot, lane);
   if (lane < 8)
     reinterpret_cast<uint4*>(k_rope + slot * kDr)[lane] = reinterpret_cast<const uint4*>(k_rope_new + tok * kDr)[lane];
+}
+
+__global__ __launch_bounds__(256) void append_kernel(const uint16_t* __restrict__ c_kv_new,
+                                                     const uint16_t* __restrict__ k_rope_new,
+                                                     const int32_t* __restrict__ page_table,
+                                                     const int32_t* __restrict__ seq_lens, int B, int n_new,
+                                                     int max_pages, int num_pages, uint8_t* __restrict__ kv_latent,
+                                                     float* __restrict__ kv_scale, uint16_t* __restrict__ k_rope) {
+  const int lane = threadIdx.x & 63;
+  const int64_t tok = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tok >= (int64_t)B * n_new) return;
+  append_token_wave(c_kv_new, k_rope_new, page_table, seq_lens, tok, n_new, max_pages, num_pages, kv_latent,
+                    kv_scale, k_rope, lane);
 }
 
 __global__ __launch_bounds__(256) void encode_kernel(const float* __restrict__ x, int64_t n,
@@ -157,8 +169,16 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
     }
     return;
   }
-  const int64_t nw = (int64_t)(gridDim.x - 1) * 4;
-  for (int64_t r = (int64_t)(blockIdx.x - 1) * 4 + (tid >> 6); r < a.rows; r += nw)
+  if ((int)blockIdx.x <= a.ablocks) {              // fused quantize-on-append
+    const int64_t tok = (int64_t)(blockIdx.x - 1) * 4 + (tid >> 6);
+    if (tok < (int64_t)a.B * a.n_new)
+      append_token_wave(a.c_kv_new, a.k_rope_new, a.page_table, a.seq_lens, tok, a.n_new, a.max_pages, a.num_pages,
+                        a.kv_latent, a.kv_scale, a.k_rope, lane);
+    return;
+  }
+  const int q0 = 1 + a.ablocks;                    // first query-quantization workgroup
+  const int64_t nw = (int64_t)(gridDim.x - q0) * 4;
+  for (int64_t r = (int64_t)(blockIdx.x - q0) * 4 + (tid >> 6); r < a.rows; r += nw)
     quantize_row_wave(a.q_nope + r * kDc, a.q8 + r * kDc, a.sq + r, lane);
 }
 
@@ -196,7 +216,8 @@ hipError_t launch_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t 
 
 hipError_t launch_prep(const PrepArgs& a, hipStream_t stream) {
   const int qblocks = a.rows > 0 ? grid_for(a.rows) : 0;
-  hipLaunchKernelGGL(prep_kernel, dim3(1 + qblocks), dim3(256), 0, stream, a);
+  if ((int64_t)1 + a.ablocks + qblocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(prep_kernel, dim3(1 + a.ablocks + qblocks), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

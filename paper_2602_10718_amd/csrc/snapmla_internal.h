@@ -26,6 +26,15 @@ struct PrepArgs {
   uint8_t* zero;            // 1 KiB that the decode kernel reads in place of slots past a sequence end
   int32_t* desc;            // [units][kDescInts] start descriptor of each split unit (see kDesc*)
   int B, q_len, max_pages, chunk_blocks, num_splits, units;
+  // optional fused quantize-on-append of n_new tokens per sequence (ablocks workgroups of
+  // four tokens; none when ablocks == 0), run beside the query quantization
+  const uint16_t* c_kv_new = nullptr;   // [B][n_new][512]
+  const uint16_t* k_rope_new = nullptr; // [B][n_new][64]
+  const int32_t* page_table = nullptr;
+  uint8_t* kv_latent = nullptr;
+  float* kv_scale = nullptr;
+  uint16_t* k_rope = nullptr;
+  int n_new = 0, num_pages = 0, ablocks = 0;
 };
 
 // Start descriptor of a split unit (a workgroup's range of 64-token blocks), written

@@ -1,8 +1,9 @@
 """Device-side staging for a decode workload: cache planes, queries, workspace, and one step.
 
 A step is the whole hot path for one batch: quantize-and-append the step's new
-tokens, quantize the queries and decode (snapmla_decode), and merge the KV
-pieces (snapmla_combine).  Everything runs in libsnapmla.so; torch only owns
+tokens, quantize the queries and decode (one snapmla_append_decode call: the
+append runs in the decode's preparation launch), and merge the KV pieces
+(snapmla_combine).  Everything runs in libsnapmla.so; torch only owns
 the device buffers and the stream.
 """
 
@@ -121,9 +122,18 @@ class DecodeRunner:
         sm.snapmla_combine(self.workspace, self.seq_lens, self.B, self.q_len, self.H, self.num_splits,
                            self.kv_chunk_tokens, self.out, self.lse, stream=stream)
 
+    def append_decode(self, stream=None):
+        """The step's append and decode in one call (the append runs in the decode's preparation launch)."""
+        sm.snapmla_append_decode(self.new_ckv, self.new_krope, self.q_nope, self.q_rope, self.kv_latent, self.kv_scale,
+                                 self.k_rope, self.page_table, self.seq_lens, self.wl.tau, self.wl.causal,
+                                 self.num_splits, self.kv_chunk_tokens, self.workspace, stream=stream)
+
     def step(self, stream=None):
-        self.append(stream)
-        self.decode(stream)
+        if self.kv_dtype == "bf16":
+            self.append(stream)
+            self.decode(stream)
+        else:
+            self.append_decode(stream)
         self.combine(stream)
 
     def sequence_cache(self, b):

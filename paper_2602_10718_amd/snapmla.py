@@ -57,13 +57,16 @@ lib.snapmla_append_bf16.restype = ctypes.c_int
 lib.snapmla_append_bf16.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p]
 lib.snapmla_fetch_dequant.restype = ctypes.c_int
 lib.snapmla_fetch_dequant.argtypes = [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]
+lib.snapmla_append_decode.restype = ctypes.c_int
+lib.snapmla_append_decode.argtypes = [_p, _p, _i32, _p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32,
+                                      _f32, _i32, _i32, _i32, _p, _sz, _p]
 lib.snapmla_debug_read_ceiling.restype = ctypes.c_int
 lib.snapmla_debug_read_ceiling.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p]
 
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
            "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16",
-           "snapmla_debug_read_ceiling"]
+           "snapmla_debug_read_ceiling", "snapmla_append_decode"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -145,6 +148,19 @@ def snapmla_decode(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_
                               _ptr(page_table), _ptr(seq_lens), B, q_len, H, page_table.shape[1], kv_latent.shape[0],
                               page_size, float(softmax_scale), int(causal), num_splits, kv_chunk_tokens,
                               _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def snapmla_append_decode(c_kv_new, k_rope_new, q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens,
+                          softmax_scale, causal, num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None):
+    """snapmla_quantize_append of c_kv_new bf16 [B, n_new, 512] / k_rope_new bf16 [B, n_new, 64] followed by
+    snapmla_decode, the append run in the decode's preparation launch."""
+    B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
+    n_new = c_kv_new.shape[1]
+    _check(lib.snapmla_append_decode(_ptr(c_kv_new), _ptr(k_rope_new), n_new, _ptr(q_nope), _ptr(q_rope),
+                                     _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope), _ptr(page_table), _ptr(seq_lens),
+                                     B, q_len, H, page_table.shape[1], kv_latent.shape[0], page_size,
+                                     float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def snapmla_combine(workspace, seq_lens, B, q_len, H, num_splits, kv_chunk_tokens, out, lse=None, stream=None):

@@ -148,3 +148,19 @@ def test_read_ceiling_validates(sm):
     assert L.snapmla_debug_read_ceiling(4104, 4096, 4096, 4096, 10, 4, 1, 4096, None) == 4        # misaligned plane
     assert L.snapmla_debug_read_ceiling(4096, 4096, 4096, 4098, 10, 4, 1, 4096, None) == 4        # misaligned pages
 
+
+
+def test_append_decode_validates(sm):
+    L = sm.lib
+    big = 1 << 30
+    # n_new < 0; then the decode's own checks (q_len 3); then null / misaligned new-token pointers
+    assert L.snapmla_append_decode(None, None, -1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
+                                   0.1, 0, 8, 0, 4096, big, None) == 1
+    assert L.snapmla_append_decode(4096, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 3, 16, 4, 8, 64,
+                                   0.1, 0, 8, 0, 4096, big, None) == 1
+    assert L.snapmla_append_decode(None, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
+                                   0.1, 0, 8, 0, 4096, big, None) == 1
+    assert L.snapmla_append_decode(4104, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
+                                   0.1, 0, 8, 0, 4096, big, None) == 4
+    assert L.snapmla_append_decode(None, None, 1, None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64,
+                                   0.1, 0, 8, 0, None, 0, None) == 0                            # B == 0

@@ -148,3 +148,23 @@ def test_plan_with_many_sequences_and_units():
             assert np.all(out[b] == 0) and np.all(lse[b] == -np.inf)
         for b in (0, 1, 4, 6, 76, 78, 149, 151, 255, 256, 257, 299):
             check_sequence(run, b, reference(w, b, qn, qr), label=f"many-seq {kw}")
+
+
+@pytest.mark.parametrize("name", ["ragged-h16", "h128-two-rowgroups", "mtp-causal-r256", "fixed-chunks-causal"])
+def test_append_decode_equals_separate_calls(name):
+    """snapmla_append_decode (append inside the preparation launch) against snapmla_quantize_append
+    followed by snapmla_decode: the same cache bytes, outputs and LSEs, bit for bit."""
+    fac, kw = CASES[name]
+    w = fac()
+    fused, split = runner(w, **kw), runner(w, **kw)
+    print(f"[append_decode] {name}", flush=True)
+    fused.append_decode()
+    fused.combine()
+    split.append()
+    split.decode()
+    split.combine()
+    torch.cuda.synchronize()
+    for a, b in ((fused.kv_latent, split.kv_latent), (fused.kv_scale, split.kv_scale), (fused.k_rope, split.k_rope)):
+        assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
+    assert torch.equal(fused.out.view(torch.int32), split.out.view(torch.int32))
+    assert torch.equal(fused.lse.view(torch.int32), split.lse.view(torch.int32))
