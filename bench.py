@@ -285,17 +285,22 @@ def bench_bf16(args, w, run8):
         return (float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3,
                 float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) * 1e3)
 
+    # both legs as three calls (append, decode, combine), so that the two steps have the same
+    # launch structure (the FP8 path's fused snapmla_append_decode has no BF16 counterpart)
+    def split_step(run):
+        return lambda: (run.append(), run.decode(), run.combine())
+
     res = {}
     for name, run in (("fp8", run8), ("bf16", run16)):
         for _ in range(args.warmup):
-            run.step()
-        step_us = timed(run.step, args.steps)
+            split_step(run)()
+        step_us = timed(split_step(run), args.steps)
         dec_us, comb_us = per_call(run)
         res[name] = {"step_us": round(step_us, 1), "decode_us": round(dec_us, 1), "combine_us": round(comb_us, 1)}
         _log(f"{name}: step {step_us:.1f} us, decode {dec_us:.1f} us, combine {comb_us:.1f} us")
     # interleaved repeat, so that a clock drift between the two legs does not decide the ratio
-    f8b = [timed(run8.step, args.steps) for _ in range(3)]
-    b16b = [timed(run16.step, args.steps) for _ in range(3)]
+    f8b = [timed(split_step(run8), args.steps) for _ in range(3)]
+    b16b = [timed(split_step(run16), args.steps) for _ in range(3)]
     kv16 = w.total_tokens * BF16_BYTES_PER_TOKEN
     kv8 = w.kv_bytes()
     us16 = res["bf16"]["step_us"]
@@ -311,7 +316,7 @@ def bench_bf16(args, w, run8):
         "config": {"workload": wl_describe(args.workload) + ", BF16 cache (1152 B per token)", "batch": w.B,
                    "heads": w.H, "q_len": w.q_len, "kv_tokens": w.total_tokens, "kv_bytes_bf16": kv16,
                    "kv_bytes_fp8": kv8, "num_splits": run16.num_splits,
-                   "step": "append_bf16 + decode_bf16 + combine"},
+                   "step": "append_bf16 + decode_bf16 + combine (FP8 leg: quantize_append + decode + combine), three calls each"},
         "fp8": res["fp8"], "bf16": res["bf16"],
         "speedup_fp8_over_bf16": {"step": round(us16 / res["fp8"]["step_us"], 3),
                                   "decode_call": round(dec16 / res["fp8"]["decode_us"], 3),
