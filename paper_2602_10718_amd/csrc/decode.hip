@@ -210,13 +210,14 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     for (int s = 0; s < 2; ++s) roff[s] = (uint32_t)(n16 * (kDr * 2) + (((4 * s + g4) ^ (n16 >> 1)) << 4));
     const uint32_t soff = (uint32_t)(kRopeBytes + 16 * g4);
 
-    // queries and fresh row state of the current piece: for the first piece before
-    // the first barrier, for later ones right after the previous piece's last block
-    // was published, so the loads overlap the wait at the barrier
-    auto start_piece = [&]() {
-      vis = a.causal ? cur_n - a.q_len + 1 + row / a.H : cur_n;
+    // queries of a piece: for the first piece before the first barrier; for a later
+    // one right after the previous piece's last block was published (its queries are
+    // no longer read), so the loads overlap the wait at the barrier.  The later
+    // piece's bounds are fetched two blocks ahead, after a publication as well, so
+    // the scalar round trip is not on the query loads' path.
+    auto load_q = [&](int qb) {
       if (row_ok) {
-        const int64_t qrow = (int64_t)cur_b * a.R + row;
+        const int64_t qrow = (int64_t)qb * a.R + row;
         const v4i* src = reinterpret_cast<const v4i*>(a.q8 + qrow * kDc);
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
@@ -234,17 +235,26 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         for (int s = 0; s < 2; ++s) qr[s] = v4i{0, 0, 0, 0};
         cq = 0.f;
       }
+    };
+    auto reset_rows = [&]() {
+      vis = a.causal ? cur_n - a.q_len + 1 + row / a.H : cur_n;
       m = -INFINITY; sp = 1.0f; l = 0.0f;
     };
-    start_piece();
+    load_q(cur_b);
+    reset_rows();
+    bool nx_ready = false, q_ready = false;   // next piece's bounds fetched / its queries loaded
 
     for (int k = 0; k < nblocks; ++k) {
       barrier_vm_lgkm0<63>();                              // page k has landed (PV waves waited)
       const int gb = gstart + k;
       if (gb >= cur_end) {                                 // first block of a later piece
-        fetch_next(gb);
+        if (!q_ready) {
+          if (!nx_ready) fetch_next(gb);
+          load_q(nx_b);
+        }
         take_next(gb);
-        start_piece();
+        reset_rows();
+        nx_ready = q_ready = false;
       }
       const int blk = gb - cur_p0;
       const uint8_t* st = smem + (k % kLatStages) * kLatBytes;             // latent of block k
@@ -352,6 +362,16 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       if (g4 == 0) *reinterpret_cast<v4f*>(xg + (16 * w + n16) * 4) = v4f{gam, l, m, sp};
       lds_wait_all();
       if (lane == 0) flag_store(xf + w, k + 1);   // block k published
+      if (cur_end < gend) {                        // a later piece starts inside the range
+        if (!nx_ready && gb + 2 >= cur_end) {
+          fetch_next(cur_end);
+          nx_ready = true;
+        }
+        if (gb + 1 == cur_end) {                   // this piece's queries are no longer read
+          load_q(nx_b);
+          q_ready = true;
+        }
+      }
     }
     barrier_vm_lgkm0<63>();                        // pairs with the PV waves' last top barrier
   } else {
