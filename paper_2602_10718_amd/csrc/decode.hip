@@ -24,16 +24,20 @@
 // output half.)
 //
 // Data movement: each 64-token page (32 KiB E4M3 latent, 8 KiB bf16 RoPE,
-// 256 B scales) is copied HBM -> LDS with 16-byte direct-to-LDS loads right
-// after the barrier that opens a period: the latent three blocks ahead of the QK
-// waves, the RoPE/scale part two.  The latent lives four periods in LDS (three
-// arriving, one in use) and the RoPE/scale part three, hence a 4-stage latent
-// ring and a 3-stage RoPE/scale ring (160 KiB of LDS in all).  Latent rows are
+// 256 B scales) is copied HBM -> LDS with 16-byte direct-to-LDS loads, issued
+// once per period by the PV waves (after the products of block k-1 with one row
+// group, right after the barrier with several): the latent three blocks ahead of
+// the QK waves, the RoPE/scale part two.  The latent lives four periods in LDS
+// (three arriving, one in use) and the RoPE/scale part three, hence a 4-stage
+// latent ring and a 3-stage RoPE/scale ring (158 KiB of LDS in all).  Latent rows are
 // stored with the 16-byte chunk index XOR-swizzled by the token index (swz) so
 // that both the token-major QK reads and the transposed PV reads avoid bank
-// conflicts.  Page ids travel the same way, four blocks ahead of their copy.
-// A workgroup starts from the descriptor of its block range that the prep kernel
-// wrote (range and first sequence): no search of the split plan.
+// conflicts.  Page ids travel the same way, requested three periods before the
+// latent copy that uses them.  A workgroup starts from the descriptor of its block
+// range that the prep kernel wrote (range and first sequence): no search of the
+// split plan.  When the range crosses into another sequence, the QK waves fetch
+// its bounds two blocks ahead and load its queries right after publishing the
+// previous sequence's last block.
 // Two PV-wave schedules (template flag kRotate, chosen by the launch): with one
 // row group, products of block k-1 first, then the copies, then the transposed
 // reads of block k into the same registers; with several row groups (pages shared
