@@ -168,3 +168,38 @@ def test_append_decode_equals_separate_calls(name):
         assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
     assert torch.equal(fused.out.view(torch.int32), split.out.view(torch.int32))
     assert torch.equal(fused.lse.view(torch.int32), split.lse.view(torch.int32))
+
+
+def test_append_decode_data_errors_and_no_append_equal_separate_calls():
+    """The fused call on data errors (an out-of-range page id under the new tokens, an empty
+    sequence, 0 < seq_len < q_len) and with n_new = 0 matches the separate calls bit for bit."""
+    w = wl.custom(B=5, H=16, q_len=2, seq_lens=[0, 130, 70, 1, 64], causal=True, seed=34, n_new=2)
+    fused, split = runner(w, num_splits=8), runner(w, num_splits=8)
+    for r in (fused, split):
+        pt = r.page_table.clone()
+        pt[1, 2] = w.num_pages + 3            # the page of sequence 1's new tokens
+        r.page_table = pt
+    print("[append_decode] data errors", flush=True)
+    fused.append_decode()
+    fused.combine()
+    split.append()
+    split.decode()
+    split.combine()
+    torch.cuda.synchronize()
+    for a, b in ((fused.kv_latent, split.kv_latent), (fused.kv_scale, split.kv_scale), (fused.k_rope, split.k_rope)):
+        assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
+    assert torch.equal(fused.out.view(torch.int32), split.out.view(torch.int32))
+    assert torch.equal(fused.lse.view(torch.int32), split.lse.view(torch.int32))
+    assert np.all(np.isnan(fused.out[1].float().cpu().numpy()))
+
+    w0 = wl.custom(B=3, H=64, q_len=1, seq_lens=[300, 64, 129], seed=35, n_new=0)
+    fused, split = runner(w0, num_splits=8), runner(w0, num_splits=8)
+    assert fused.new_ckv.shape[1] == 0
+    print("[append_decode] n_new = 0", flush=True)
+    fused.append_decode()
+    fused.combine()
+    split.decode()
+    split.combine()
+    torch.cuda.synchronize()
+    assert torch.equal(fused.out.view(torch.int32), split.out.view(torch.int32))
+    assert torch.equal(fused.lse.view(torch.int32), split.lse.view(torch.int32))
