@@ -45,7 +45,8 @@ class DecodeRunner:
             if self.kv_chunk_tokens > 0:
                 num_splits = max(1, int(np.max((wl.seq_lens + self.kv_chunk_tokens - 1) // self.kv_chunk_tokens)))
             else:
-                num_splits = sm.default_num_splits(self.q_len, self.H)
+                num_splits = sm.default_num_splits(self.q_len, self.H,
+                                                   total_blocks=int(((wl.seq_lens.astype(np.int64) + 63) // 64).sum()))
         self.num_splits = num_splits
         P = wl.num_pages
         if cache is not None:

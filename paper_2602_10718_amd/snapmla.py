@@ -175,11 +175,16 @@ def snapmla_combine(workspace, seq_lens, B, q_len, H, num_splits, kv_chunk_token
                                q_len, H, num_splits, kv_chunk_tokens, _ptr(out), od, _ptr(lse), _stream(stream)))
 
 
-def default_num_splits(q_len, H, device=None):
-    """One workgroup per compute unit across all row groups, rounded down to a multiple of 8."""
+def default_num_splits(q_len, H, device=None, total_blocks=None):
+    """One workgroup per compute unit across all row groups, rounded down to a multiple of 8; with
+    total_blocks (the batch's 64-token blocks) given, no more parts than blocks (rounded up to a
+    multiple of 8), so that a small batch launches no idle parts for the combine to step over."""
     props = torch.cuda.get_device_properties(device if device is not None else torch.cuda.current_device())
     groups = math.ceil(q_len * H / 64)
-    return max(8, (props.multi_processor_count // groups) // 8 * 8)
+    n = max(8, (props.multi_processor_count // groups) // 8 * 8)
+    if total_blocks is not None:
+        n = min(n, max(8, (int(total_blocks) + 7) // 8 * 8))
+    return n
 
 
 def snapmla_fetch_dequant(kv_latent, kv_scale, k_rope, page_table, cu_seqlens, out, page_size=64, stream=None):
