@@ -90,11 +90,28 @@ def cpu_baseline(w, budget_s=15.0):
         seqs += 1
         if el > budget_s and seqs >= 2:
             break
-    return {"value": round(toks * BYTES_PER_TOKEN / el / 1e9, 3), "unit": "GB/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{seqs} of {w.B} sequences ({toks} KV tokens, {w.H * w.q_len} rows each): per-token "
-                      f"quantization + decode_streaming in float64, {el:.1f} s; the full step extrapolates to "
-                      f"{el * w.total_tokens / toks:.1f} s"}
+    res = {"value": round(toks * BYTES_PER_TOKEN / el / 1e9, 3), "unit": "GB/s", "cores": threads,
+           "kind": "oracle",
+           "sample": f"{seqs} of {w.B} sequences ({toks} KV tokens, {w.H * w.q_len} rows each): per-token "
+                     f"quantization + decode_streaming in float64, {el:.1f} s; the full step extrapolates to "
+                     f"{el * w.total_tokens / toks:.1f} s"}
+    # the same oracle with one BLAS thread, on the first sequence
+    try:
+        from threadpoolctl import threadpool_limits
+        N = int(w.seq_lens[0])
+        ck, kr = w.tokens(0, 0, N)
+        with threadpool_limits(limits=1):
+            ts = time.perf_counter()
+            q8, sq = quant.quantize_rows(qn[0].reshape(-1, 512))
+            c8, sk = quant.quantize_rows(ck)
+            mla.decode_streaming(q8, sq, qr[0].reshape(-1, 64), c8, sk, kr, w.tau,
+                                 mla.visible_counts(N, w.q_len, w.H, w.causal))
+            el1 = time.perf_counter() - ts
+        res["one_thread"] = {"value": round(N * BYTES_PER_TOKEN / el1 / 1e9, 4), "unit": "GB/s",
+                             "sample": f"sequence 0 ({N} KV tokens), {el1:.1f} s"}
+    except Exception:  # pragma: no cover
+        pass
+    return res
 
 
 FETCH_BYTES_PER_TOKEN = BYTES_PER_TOKEN + 2 * (512 + 64)     # cache row read + bf16 row written
