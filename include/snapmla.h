@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define SNAPMLA_ABI_VERSION 1
+#define SNAPMLA_ABI_VERSION 2
 
 enum snapmla_status {
   SNAPMLA_OK = 0,
@@ -66,6 +66,19 @@ enum snapmla_status {
   SNAPMLA_WORKSPACE_TOO_SMALL = 3,
   SNAPMLA_MISALIGNED = 4,         /* a pointer is not 16-byte aligned */
   SNAPMLA_HIP_ERROR = 5           /* a HIP runtime call failed */
+};
+
+/* Flags of snapmla_decode and snapmla_append_decode. */
+enum snapmla_decode_flags {
+  /* Form the content term <q8, c8> with exact float32 accumulation: the E4M3
+   * codes are converted to f16 (an exact conversion) and multiplied with the F16
+   * matrix cores.  Without it the FP8 matrix cores sum each group of eight
+   * consecutive products with every product truncated to a multiple of
+   * 2^(E-13), E the group's largest exponent sum (gfx950 behaviour, measured
+   * bit for bit), which moves logits in the thousands by up to ~1e-1 and the
+   * LSE with them.  Same inputs, outputs and workspace; slower (the conversion
+   * and twice the matrix-core work of the content term). */
+  SNAPMLA_DECODE_EXACT_QK = 1
 };
 
 /* ABI version of the loaded library (SNAPMLA_ABI_VERSION). */
@@ -151,6 +164,7 @@ int snapmla_decode_workspace_size(int32_t B, int32_t q_len, int32_t H,
  *   softmax_scale         finite, > 0
  *   causal                0 or 1 (only meaningful for q_len = 2)
  *   num_splits, kv_chunk_tokens   split plan (see snapmla_decode_workspace_size)
+ *   flags                 0 or SNAPMLA_DECODE_EXACT_QK (other bits: SNAPMLA_INVALID_ARGUMENT)
  *   workspace / workspace_bytes   device scratch of at least the queried size
  */
 int snapmla_decode(const void* q_nope, const void* q_rope,
@@ -159,7 +173,7 @@ int snapmla_decode(const void* q_nope, const void* q_rope,
                    int32_t B, int32_t q_len, int32_t H,
                    int32_t max_pages, int32_t num_pages, int32_t page_size,
                    float softmax_scale, int32_t causal,
-                   int32_t num_splits, int32_t kv_chunk_tokens,
+                   int32_t num_splits, int32_t kv_chunk_tokens, int32_t flags,
                    void* workspace, size_t workspace_bytes,
                    hipStream_t stream);
 
@@ -184,7 +198,7 @@ int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t 
                           int32_t B, int32_t q_len, int32_t H,
                           int32_t max_pages, int32_t num_pages, int32_t page_size,
                           float softmax_scale, int32_t causal,
-                          int32_t num_splits, int32_t kv_chunk_tokens,
+                          int32_t num_splits, int32_t kv_chunk_tokens, int32_t flags,
                           void* workspace, size_t workspace_bytes,
                           hipStream_t stream);
 
@@ -316,6 +330,20 @@ int snapmla_e4m3_encode(const float* x, int64_t n, uint8_t* codes, hipStream_t s
 int snapmla_debug_read_ceiling(const uint8_t* kv_latent, const float* kv_scale, const void* k_rope,
                                const int32_t* pages, int32_t nblk, int32_t num_pages, int32_t units,
                                uint32_t* out, hipStream_t stream);
+
+/*
+ * snapmla_debug_set_spin_limit -- test hook: the bound on the polls of every
+ * handshake wait inside the decode kernels of later snapmla_decode,
+ * snapmla_append_decode and snapmla_decode_bf16 calls of this process (default
+ * 4194304).  The waits end by construction; the bound only guarantees that a
+ * kernel terminates.  A wait that reaches it marks its KV piece, whose outputs
+ * and LSEs then come out NaN, so a lost handshake is visible rather than
+ * silently stale.  With polls = 0 every wait gives up at once (every output
+ * NaN), which lets a test check that path without hanging anything.
+ *   polls >= 0 (SNAPMLA_INVALID_ARGUMENT otherwise).  Process-wide; not for
+ *   concurrent use with decode calls on other threads.
+ */
+int snapmla_debug_set_spin_limit(int32_t polls);
 
 #ifdef __cplusplus
 }

@@ -1,6 +1,7 @@
 // C ABI of libsnapmla.so (declared in include/snapmla.h): argument validation,
 // workspace carve-up and kernel launches on the caller's stream.
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -12,6 +13,7 @@
 namespace {
 
 thread_local std::string g_last_error;
+std::atomic<int> g_spin_limit{snapmla::kDefaultSpinLimit};
 
 int fail(int code, const char* fmt, ...) {
   char buf[512];
@@ -70,9 +72,11 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
                   int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
                   float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
                   void* workspace, size_t workspace_bytes, hipStream_t stream, bool bf16_cache,
-                  const AppendIn& app = AppendIn()) {
+                  const AppendIn& app = AppendIn(), int32_t flags = 0) {
   int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
   if (st != SNAPMLA_OK) return st;
+  if ((flags & ~SNAPMLA_DECODE_EXACT_QK) != 0)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "unknown decode flags 0x%x", (unsigned)flags);
   if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
   if (max_pages < 1 || num_pages < 1)
     return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
@@ -156,6 +160,8 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   d.num_splits = num_splits;
   d.chunk_blocks = kv_chunk_tokens / 64;
   d.sl2 = softmax_scale * 1.4426950408889634f;
+  d.spin_limit = snapmla::spin_limit();
+  d.qk_exact = (flags & SNAPMLA_DECODE_EXACT_QK) != 0 ? 1 : 0;
   if (bf16_cache)
     return hip_status(snapmla::launch_decode_bf16(d, static_cast<const uint16_t*>(kv_latent), stream),
                       "decode_bf16 launch");
@@ -165,6 +171,8 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
 }  // namespace
 
 namespace snapmla {
+
+int spin_limit() { return g_spin_limit.load(std::memory_order_relaxed); }
 
 WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens) {
   WsLayout L;
@@ -194,6 +202,12 @@ extern "C" {
 int snapmla_abi_version(void) { return SNAPMLA_ABI_VERSION; }
 
 const char* snapmla_get_last_error(void) { return g_last_error.c_str(); }
+
+int snapmla_debug_set_spin_limit(int32_t polls) {
+  if (polls < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "polls must be >= 0 (got %d)", polls);
+  g_spin_limit.store(polls == 0 ? 0 : polls, std::memory_order_relaxed);
+  return ok();
+}
 
 int snapmla_quantize_append(const void* c_kv_new, const void* k_rope_new, const int32_t* page_table,
                             const int32_t* seq_lens, int32_t B, int32_t n_new, int32_t max_pages,
@@ -247,18 +261,18 @@ int snapmla_decode(const void* q_nope, const void* q_rope, const uint8_t* kv_lat
                    const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
                    int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
                    float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
-                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                   int32_t flags, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
                        num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
-                       workspace_bytes, stream, false);
+                       workspace_bytes, stream, false, AppendIn(), flags);
 }
 
 int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t n_new, const void* q_nope,
                           const void* q_rope, uint8_t* kv_latent, float* kv_scale, void* k_rope,
                           const int32_t* page_table, const int32_t* seq_lens, int32_t B, int32_t q_len, int32_t H,
                           int32_t max_pages, int32_t num_pages, int32_t page_size, float softmax_scale,
-                          int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens, void* workspace,
-                          size_t workspace_bytes, hipStream_t stream) {
+                          int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens, int32_t flags,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (n_new < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "n_new must be >= 0 (got %d)", n_new);
   AppendIn app;
   app.c_kv_new = c_kv_new;
@@ -266,7 +280,7 @@ int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t 
   app.n_new = n_new;
   return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
                        num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
-                       workspace_bytes, stream, false, app);
+                       workspace_bytes, stream, false, app, flags);
 }
 
 int snapmla_decode_bf16(const void* q_nope, const void* q_rope, const void* kv_latent, const void* k_rope,

@@ -43,7 +43,6 @@ constexpr int kSmem = kRingBase + 64;
 static_assert(kSmem <= 160 * 1024, "LDS budget of one workgroup");
 constexpr int kStores = 2 * (16 + 1);                   // piece-end stores of a PV wave
 static_assert(18 + kStores < 64, "wait counter range");
-constexpr int kSpin = 1 << 22;
 constexpr float kLn2f = 0.69314718055994531f;
 
 // Latent rows: 16-byte chunk c of token t at chunk c ^ swz(t).  Within 16
@@ -405,9 +404,13 @@ __global__ __launch_bounds__(512, 1) void decode_bf16_kernel(DecodeArgs a, const
             rv[T][kk][rr] = lds_read_tr16_at(st_lds + ((tr_off[rr] | (uint32_t)(kk << 14)) ^ (uint32_t)(T << 6)));
         }
       }
-      for (int spin = 0; spin < kSpin; ++spin) {
-        const v4i f4 = fload4(xf);
-        if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
+      {
+        int spin = 0;
+        for (; spin < a.spin_limit; ++spin) {
+          const v4i f4 = fload4(xf);
+          if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
+        }
+        if (spin == a.spin_limit) cur_bad = true;   // codes never published: the piece comes out NaN
       }
       asm volatile("" ::: "memory");
       gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);

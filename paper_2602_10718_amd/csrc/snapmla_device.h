@@ -46,6 +46,25 @@ __device__ __forceinline__ v4f mfma_f8_16x16x128(v8i a, v8i b, v4f c) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
+// 16x16x32 F16 MFMA: lane (i%16, i/16) holds K = 8*(i/16) + 0..7; same C layout.
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ v4f mfma_f16_16x16x32(v4i a, v4i b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(v8h, a), __builtin_bit_cast(v8h, b), c, 0, 0, 0);
+}
+
+// Four E4M3 codes (bytes of one dword) -> four halfs in two dwords.  The conversion
+// is exact: every E4M3 value, subnormals included, is a normal f16 value.
+__device__ __forceinline__ v2i e4m3x4_to_f16(int x) {
+  const auto lo = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8((unsigned)x, 1.0f, false);
+  const auto hi = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8((unsigned)x, 1.0f, true);
+  return v2i{__builtin_bit_cast(int, lo), __builtin_bit_cast(int, hi)};
+}
+// Eight codes (two dwords) -> the eight-half operand of one 16x16x32 F16 MFMA.
+__device__ __forceinline__ v4i e4m3x8_to_f16(int x0, int x1) {
+  const v2i a = e4m3x4_to_f16(x0), b = e4m3x4_to_f16(x1);
+  return v4i{a[0], a[1], b[0], b[1]};
+}
+
 // 16x16x32 BF16 MFMA: lane (i%16, i/16) holds K = 8*(i/16) + 0..7; same C layout.
 __device__ __forceinline__ v4f mfma_bf16_16x16x32(v4i a, v4i b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a), __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
@@ -148,6 +167,12 @@ __device__ __forceinline__ void g2lds4_so(const void* sbase, uint32_t voff, uint
 // values would only be spilled).
 __device__ __forceinline__ uint32_t opaque_u32(uint32_t x) {
   asm volatile("" : "+v"(x));
+  return x;
+}
+// The same for a wave-uniform value, kept in a scalar register.
+__device__ __forceinline__ uint32_t opaque_s32(uint32_t x) {
+  x = __builtin_amdgcn_readfirstlane(x);
+  asm volatile("" : "+s"(x));
   return x;
 }
 

@@ -47,6 +47,10 @@ constexpr int kDescP0 = 3;       // its first global block (prefix[seq])
 constexpr int kDescP1 = 4;       // one past its last (prefix[seq + 1])
 constexpr int kDescLen = 5;      // its length in tokens
 
+constexpr int kDefaultSpinLimit = 1 << 22;
+// process-wide spin limit of the decode launches (snapmla_debug_set_spin_limit)
+int spin_limit();
+
 struct DecodeArgs {
   const uint16_t* q_nope;   // [B*R][512] bf16 (read by the BF16-cache kernel only)
   const uint8_t* q8;
@@ -65,6 +69,14 @@ struct DecodeArgs {
   int B, q_len, H, R, G, rows_pad, max_pages, num_pages, causal;
   int num_splits, chunk_blocks;  // chunk_blocks == 0: balanced plan over num_splits parts
   float sl2;                     // softmax scale * log2(e)
+  // Upper bound on the polls of each handshake wait inside the decode kernels.  The
+  // waits end by construction (every flag they poll is stored once per block, before
+  // its owner waits on anything); the bound only guarantees termination.  A wait that
+  // reaches it marks its piece, whose outputs and LSEs then come out NaN.
+  int spin_limit = kDefaultSpinLimit;
+  // QK content product with exact float32 accumulation (F16 MFMA on the exactly
+  // converted E4M3 codes) instead of the FP8 MFMA
+  int qk_exact = 0;
 };
 
 struct CombineArgs {

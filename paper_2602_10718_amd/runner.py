@@ -33,11 +33,13 @@ class DecodeRunner:
     """
 
     def __init__(self, wl, num_splits=None, kv_chunk_tokens=None, out_dtype=torch.float32, fill=True, cache=None,
-                 kv_dtype="e4m3"):
+                 kv_dtype="e4m3", exact_qk=False):
         """cache: (kv_latent, kv_scale, k_rope) of another runner over the same sequences, pages and
         tokens, used instead of allocating and filling a new one.  kv_dtype "bf16": a BF16 cache
-        (kv_latent bf16, no scales) written by snapmla_append_bf16 and read by snapmla_decode_bf16."""
+        (kv_latent bf16, no scales) written by snapmla_append_bf16 and read by snapmla_decode_bf16.
+        exact_qk: decode with SNAPMLA_DECODE_EXACT_QK (content term accumulated exactly in float32)."""
         self.kv_dtype = kv_dtype
+        self.flags = sm.DECODE_EXACT_QK if exact_qk else 0
         self.wl = wl
         self.B, self.H, self.q_len = wl.B, wl.H, wl.q_len
         self.kv_chunk_tokens = wl.kv_chunk_tokens if kv_chunk_tokens is None else kv_chunk_tokens
@@ -117,7 +119,7 @@ class DecodeRunner:
             return
         sm.snapmla_decode(self.q_nope, self.q_rope, self.kv_latent, self.kv_scale, self.k_rope, self.page_table,
                           self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits, self.kv_chunk_tokens,
-                          self.workspace, stream=stream)
+                          self.workspace, stream=stream, flags=self.flags)
 
     def combine(self, stream=None):
         sm.snapmla_combine(self.workspace, self.seq_lens, self.B, self.q_len, self.H, self.num_splits,
@@ -127,7 +129,8 @@ class DecodeRunner:
         """The step's append and decode in one call (the append runs in the decode's preparation launch)."""
         sm.snapmla_append_decode(self.new_ckv, self.new_krope, self.q_nope, self.q_rope, self.kv_latent, self.kv_scale,
                                  self.k_rope, self.page_table, self.seq_lens, self.wl.tau, self.wl.causal,
-                                 self.num_splits, self.kv_chunk_tokens, self.workspace, stream=stream)
+                                 self.num_splits, self.kv_chunk_tokens, self.workspace, stream=stream,
+                                 flags=self.flags)
 
     def step(self, stream=None):
         if self.kv_dtype == "bf16":

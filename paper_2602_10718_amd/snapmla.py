@@ -43,7 +43,7 @@ lib.snapmla_decode_workspace_size.restype = ctypes.c_int
 lib.snapmla_decode_workspace_size.argtypes = [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
 lib.snapmla_decode.restype = ctypes.c_int
 lib.snapmla_decode.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
-                               _i32, _p, _sz, _p]
+                               _i32, _i32, _p, _sz, _p]
 lib.snapmla_combine.restype = ctypes.c_int
 lib.snapmla_combine.argtypes = [_p, _sz, _p, _i32, _i32, _i32, _i32, _i32, _p, _i32, _p, _p]
 lib.snapmla_e4m3_encode.restype = ctypes.c_int
@@ -59,14 +59,16 @@ lib.snapmla_fetch_dequant.restype = ctypes.c_int
 lib.snapmla_fetch_dequant.argtypes = [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]
 lib.snapmla_append_decode.restype = ctypes.c_int
 lib.snapmla_append_decode.argtypes = [_p, _p, _i32, _p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32,
-                                      _f32, _i32, _i32, _i32, _p, _sz, _p]
+                                      _f32, _i32, _i32, _i32, _i32, _p, _sz, _p]
 lib.snapmla_debug_read_ceiling.restype = ctypes.c_int
+lib.snapmla_debug_set_spin_limit.restype = ctypes.c_int
+lib.snapmla_debug_set_spin_limit.argtypes = [_i32]
 lib.snapmla_debug_read_ceiling.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p]
 
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
            "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16",
-           "snapmla_debug_read_ceiling", "snapmla_append_decode"]
+           "snapmla_debug_read_ceiling", "snapmla_append_decode", "snapmla_debug_set_spin_limit"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -139,19 +141,23 @@ def snapmla_decode_workspace_size(B, q_len, H, num_splits, kv_chunk_tokens):
     return out.value
 
 
+DECODE_EXACT_QK = 1   # snapmla_decode_flags: content term with exact float32 accumulation
+
+
 def snapmla_decode(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, softmax_scale, causal,
-                   num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None):
+                   num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None, flags=0):
     """q_nope bf16 [B, q_len, H, 512], q_rope bf16 [B, q_len, H, 64]; cache planes as in snapmla_quantize_append;
-    workspace uint8 of at least snapmla_decode_workspace_size(...) bytes."""
+    workspace uint8 of at least snapmla_decode_workspace_size(...) bytes; flags 0 or DECODE_EXACT_QK."""
     B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
     _check(lib.snapmla_decode(_ptr(q_nope), _ptr(q_rope), _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope),
                               _ptr(page_table), _ptr(seq_lens), B, q_len, H, page_table.shape[1], kv_latent.shape[0],
-                              page_size, float(softmax_scale), int(causal), num_splits, kv_chunk_tokens,
+                              page_size, float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, int(flags),
                               _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def snapmla_append_decode(c_kv_new, k_rope_new, q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens,
-                          softmax_scale, causal, num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None):
+                          softmax_scale, causal, num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None,
+                          flags=0):
     """snapmla_quantize_append of c_kv_new bf16 [B, n_new, 512] / k_rope_new bf16 [B, n_new, 64] followed by
     snapmla_decode, the append run in the decode's preparation launch."""
     B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
@@ -159,8 +165,8 @@ def snapmla_append_decode(c_kv_new, k_rope_new, q_nope, q_rope, kv_latent, kv_sc
     _check(lib.snapmla_append_decode(_ptr(c_kv_new), _ptr(k_rope_new), n_new, _ptr(q_nope), _ptr(q_rope),
                                      _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope), _ptr(page_table), _ptr(seq_lens),
                                      B, q_len, H, page_table.shape[1], kv_latent.shape[0], page_size,
-                                     float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, _ptr(workspace),
-                                     workspace.numel() * workspace.element_size(), _stream(stream)))
+                                     float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, int(flags),
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def snapmla_combine(workspace, seq_lens, B, q_len, H, num_splits, kv_chunk_tokens, out, lse=None, stream=None):
@@ -224,3 +230,8 @@ def snapmla_append_bf16(c_kv_new, k_rope_new, page_table, seq_lens, num_pages, k
     _check(lib.snapmla_append_bf16(_ptr(c_kv_new), _ptr(k_rope_new), _ptr(page_table), _ptr(seq_lens), B, n_new,
                                    page_table.shape[1], num_pages, page_size, _ptr(kv_latent), _ptr(k_rope),
                                    _stream(stream)))
+
+
+def snapmla_debug_set_spin_limit(polls):
+    """Bound on the polls of every handshake wait in later decode calls (test hook; see include/snapmla.h)."""
+    _check(lib.snapmla_debug_set_spin_limit(int(polls)))

@@ -36,7 +36,12 @@ def test_every_declared_symbol_is_exported(sm):
 
 
 def test_abi_version(sm):
-    assert sm.snapmla_abi_version() == 1
+    assert sm.snapmla_abi_version() == 2
+
+
+def test_spin_limit_hook_validates(sm):
+    assert sm.lib.snapmla_debug_set_spin_limit(-1) == 1
+    assert sm.lib.snapmla_debug_set_spin_limit(1 << 22) == 0
 
 
 def test_workspace_size_layout(sm):
@@ -64,28 +69,32 @@ def test_workspace_size_rejects(sm, args, status):
 def test_decode_argument_errors_before_any_launch(sm):
     L = sm.lib
     # unsupported page size
-    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, None, 0, None)
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, 0, None, 0, None)
     assert st == 2
     # bad softmax scale
-    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, float("nan"), 0, 8, 0, None, 0,
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, float("nan"), 0, 8, 0, 0, None, 0,
                           None)
     assert st == 1
     # null pointers
-    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0, None)
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, None, 0, None)
     assert st == 1 and "null" in sm.snapmla_get_last_error()
     # misaligned pointer (never dereferenced: validation fails first)
     p = 16 * 1024 + 8
-    st = L.snapmla_decode(p, p, p, p, p, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096, 1 << 30, None)
+    st = L.snapmla_decode(p, p, p, p, p, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096, 1 << 30, None)
     assert st == 4
     # workspace too small
-    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096, 16, None)
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096, 16, None)
     assert st == 3
     # causal flag
-    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 7, 8, 0, 4096, 1 << 30,
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 7, 8, 0, 0, 4096, 1 << 30,
                           None)
     assert st == 1
+    # unknown decode flags
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 2, 4096,
+                          1 << 30, None)
+    assert st == 1 and "flags" in sm.snapmla_get_last_error()
     # empty batch is a no-op
-    assert L.snapmla_decode(None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+    assert L.snapmla_decode(None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, None, 0,
                             None) == 0
 
 
@@ -155,12 +164,12 @@ def test_append_decode_validates(sm):
     big = 1 << 30
     # n_new < 0; then the decode's own checks (q_len 3); then null / misaligned new-token pointers
     assert L.snapmla_append_decode(None, None, -1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 4096, big, None) == 1
+                                   0.1, 0, 8, 0, 0, 4096, big, None) == 1
     assert L.snapmla_append_decode(4096, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 3, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 4096, big, None) == 1
+                                   0.1, 0, 8, 0, 0, 4096, big, None) == 1
     assert L.snapmla_append_decode(None, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 4096, big, None) == 1
+                                   0.1, 0, 8, 0, 0, 4096, big, None) == 1
     assert L.snapmla_append_decode(4104, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 4096, big, None) == 4
+                                   0.1, 0, 8, 0, 0, 4096, big, None) == 4
     assert L.snapmla_append_decode(None, None, 1, None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, None, 0, None) == 0                            # B == 0
+                                   0.1, 0, 8, 0, 0, None, 0, None) == 0                            # B == 0
