@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libsnapmla.so")
 SOURCES = ["api.hip", "quant.hip", "decode.hip", "combine.hip", "fetch.hip", "ablation.hip", "decode_bf16.hip",
-           "ceiling.hip"]
+           "ceiling.hip", "debug.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

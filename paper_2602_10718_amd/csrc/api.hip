@@ -203,6 +203,15 @@ int snapmla_abi_version(void) { return SNAPMLA_ABI_VERSION; }
 
 const char* snapmla_get_last_error(void) { return g_last_error.c_str(); }
 
+int snapmla_debug_mfma_fp8(const uint8_t* a, const uint8_t* b, float* c, int64_t tiles, hipStream_t stream) {
+  if (tiles < 0 || tiles > 0x7FFFFFFF) return fail(SNAPMLA_INVALID_ARGUMENT, "tiles out of range (got %lld)",
+                                                   (long long)tiles);
+  if (tiles == 0) return ok();
+  if (!a || !b || !c) return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(a) || misaligned(b) || misaligned(c)) return fail(SNAPMLA_MISALIGNED, "pointers must be 16-byte aligned");
+  return hip_status(snapmla::launch_mfma_fp8(a, b, c, tiles, stream), "mfma_fp8 launch");
+}
+
 int snapmla_debug_set_spin_limit(int32_t polls) {
   if (polls < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "polls must be >= 0 (got %d)", polls);
   g_spin_limit.store(polls == 0 ? 0 : polls, std::memory_order_relaxed);

@@ -119,6 +119,9 @@ hipError_t launch_quantize_cache_config(const uint16_t* c_kv, const uint16_t* k_
                                         uint32_t* amax_word, uint8_t* kv_latent, float* kv_scale,
                                         uint16_t* k_rope_out, hipStream_t stream);
 
+// One FP8 16x16x128 MFMA per 16x128 tile pair (test hook of the QK content term).
+hipError_t launch_mfma_fp8(const uint8_t* a, const uint8_t* b, float* c, int64_t tiles, hipStream_t stream);
+
 // Read-stream ceiling (measurement): the pages of nblk blocks streamed into LDS.
 constexpr int kCeilingMaxBlocks = 1792;   // blocks per workgroup (their page ids sit in LDS)
 struct CeilingArgs {

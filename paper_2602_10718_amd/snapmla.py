@@ -61,6 +61,8 @@ lib.snapmla_append_decode.restype = ctypes.c_int
 lib.snapmla_append_decode.argtypes = [_p, _p, _i32, _p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32,
                                       _f32, _i32, _i32, _i32, _i32, _p, _sz, _p]
 lib.snapmla_debug_read_ceiling.restype = ctypes.c_int
+lib.snapmla_debug_mfma_fp8.restype = ctypes.c_int
+lib.snapmla_debug_mfma_fp8.argtypes = [_p, _p, _p, _i64, _p]
 lib.snapmla_debug_set_spin_limit.restype = ctypes.c_int
 lib.snapmla_debug_set_spin_limit.argtypes = [_i32]
 lib.snapmla_debug_read_ceiling.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p]
@@ -68,7 +70,8 @@ lib.snapmla_debug_read_ceiling.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p,
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
            "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16",
-           "snapmla_debug_read_ceiling", "snapmla_append_decode", "snapmla_debug_set_spin_limit"]
+           "snapmla_debug_read_ceiling", "snapmla_append_decode", "snapmla_debug_set_spin_limit",
+           "snapmla_debug_mfma_fp8"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -235,3 +238,8 @@ def snapmla_append_bf16(c_kv_new, k_rope_new, page_table, seq_lens, num_pages, k
 def snapmla_debug_set_spin_limit(polls):
     """Bound on the polls of every handshake wait in later decode calls (test hook; see include/snapmla.h)."""
     _check(lib.snapmla_debug_set_spin_limit(int(polls)))
+
+
+def snapmla_debug_mfma_fp8(a, b, c, stream=None):
+    """a, b uint8 [tiles, 16, 128] E4M3 codes; c float32 [tiles, 16, 16] = one FP8 MFMA per tile."""
+    _check(lib.snapmla_debug_mfma_fp8(_ptr(a), _ptr(b), _ptr(c), a.shape[0], _stream(stream)))

@@ -9,7 +9,7 @@ import torch
 from oracle import granularity as gr, mla
 from paper_2602_10718_amd import snapmla as sm
 from paper_2602_10718_amd import workloads as wl
-from gpu_common import runner, check_sequence
+from gpu_common import runner, check_sequence, qk_mode
 from oracle import check
 
 pytestmark = pytest.mark.gpu
@@ -72,8 +72,9 @@ def test_decode_on_config_cache(config):
     caches = gr.quantize(config, seqs)
     for b in range(w.B):
         ck, kr = seqs[b]
-        ref = check.sequence_reference(qn[b], qr[b], ck, kr, w.tau, w.q_len, w.H, w.causal, cache=caches[b])
-        check_sequence(run, b, ref, strict_north_star=False, label=f"abl-{config}")
+        ref = check.sequence_reference(qn[b], qr[b], ck, kr, w.tau, w.q_len, w.H, w.causal, cache=caches[b],
+                                       qk=qk_mode(run))
+        check_sequence(run, b, ref, label=f"abl-{config}")
 
 
 def test_torch_reference_matches_oracle():

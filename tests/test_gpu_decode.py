@@ -40,14 +40,18 @@ CASES = {
 }
 
 
+@pytest.mark.parametrize("qk", ["mfma8", "exact"])
 @pytest.mark.parametrize("name", list(CASES))
-def test_decode_matches_oracle(name):
+def test_decode_matches_oracle(name, qk):
+    """Both QK modes: the default decode (content term on the FP8 matrix cores) against the oracle
+    that forms the content term the same way, the SNAPMLA_DECODE_EXACT_QK decode against the exact
+    oracle; each within the derived bounds and the benchmark spec tolerance."""
     fac, kw = CASES[name]
     w = fac()
-    run = _run(w, **kw)
+    run = _run(w, exact_qk=(qk == "exact"), **kw)
     qn, qr = w.queries()
     for b in range(w.B):
-        ref = reference(w, b, qn, qr)
+        ref = reference(w, b, qn, qr, qk=qk)
         check_sequence(run, b, ref, label=name)
 
 
@@ -203,3 +207,30 @@ def test_append_decode_data_errors_and_no_append_equal_separate_calls():
     torch.cuda.synchronize()
     assert torch.equal(fused.out.view(torch.int32), split.out.view(torch.int32))
     assert torch.equal(fused.lse.view(torch.int32), split.lse.view(torch.int32))
+
+
+@pytest.mark.parametrize("kv_dtype", ["e4m3", "bf16"])
+def test_handshake_wait_that_gives_up_marks_the_piece_nan(kv_dtype):
+    """A bounded handshake wait that reaches its limit must not let stale codes through silently:
+    with the limit set to 0 polls (a host-side setting; every kernel still runs to completion)
+    every piece is marked and every output and LSE comes out NaN; with the default limit the
+    same runner is back to the oracle's results."""
+    from paper_2602_10718_amd import snapmla as sm
+    w = wl.custom(B=2, H=64, q_len=1, seq_lens=[300, 200], seed=41)
+    run = runner(w, num_splits=4, kv_dtype=kv_dtype)
+    try:
+        sm.snapmla_debug_set_spin_limit(0)
+        run.step()
+        torch.cuda.synchronize()
+        assert torch.isnan(run.out).all() and torch.isnan(run.lse).all()
+    finally:
+        sm.snapmla_debug_set_spin_limit(1 << 22)
+    run.decode()
+    run.combine()
+    torch.cuda.synchronize()
+    assert torch.isfinite(run.out).all() and torch.isfinite(run.lse).all()
+    if kv_dtype == "e4m3":
+        qn, qr = w.queries()
+        for b in range(w.B):
+            check_sequence(run, b, reference(w, b, qn, qr), label="after-give-up")
+

@@ -2,6 +2,7 @@
 
 import numpy as np
 
+from paper_2602_10718_amd import workloads as wl
 from oracle import e4m3, quant
 from paper_2602_10718_amd.workloads import f32_to_bf16_bits, bf16_bits_to_f32
 
@@ -68,3 +69,40 @@ def test_zero_row_and_tiny_row():
     bits[0, 0] = f32_to_bf16_bits(np.array([300 * 2.0 ** -40], np.float32))[0]
     c, s = quant.quantize_rows(bits)
     assert s[0] == quant.EPS and e4m3.decode(c[0, 0]) == 288.0   # 300 rounds to 288 on the grid
+
+
+def test_two_roundings_reading():
+    """The quantizer rounds the float32 quotient x / sigma to E4M3 (two roundings), not the exact
+    quotient.  A constructed bf16 row where the readings differ: amax 260 gives sigma =
+    fp32(260 / 448) = 0.58035713..., slightly below 65/112, so 195 / sigma lies just above 336 --
+    the midpoint between the E4M3 values 320 (mantissa 2, even) and 352.  In float32 the quotient
+    rounds to exactly 336, a tie that goes to 320; rounded once it would give 352."""
+    row = np.zeros(512, np.float32)
+    row[0], row[1] = 260.0, 195.0
+    codes, sigma = quant.quantize_rows(wl.f32_to_bf16_bits(row)[None])
+    assert sigma[0] == np.float32(260.0) / np.float32(448.0)
+    assert np.float32(np.float32(195.0) / sigma[0]) == np.float32(336.0)      # the float32 quotient: a tie
+    assert 195.0 / float(sigma[0]) > 336.0                                     # the exact one: above it
+    assert codes[0, 0] == 0x7E                                                  # 448
+    assert e4m3.decode(codes[0, 1:2])[0] == 320.0
+    assert codes[0, 1] == 0x7A                                                  # 0 1111 010: 1.25 * 2^8
+
+
+def test_metrics_closed_forms():
+    from oracle import check
+    rng = np.random.default_rng(5)
+    o = rng.standard_normal((6, 512))
+    lse = rng.standard_normal(6) * 10
+    m = check.metrics(o * 1.01, lse + 0.25, o, lse)
+    assert abs(m["rel_l2"] - 0.01) < 1e-12
+    assert abs(m["one_minus_cos"]) < 1e-12
+    assert abs(m["lse_max_abs"] - 0.25) < 1e-12
+    assert abs(m["max_abs"] - 0.01 * np.max(np.abs(o))) < 1e-12
+    assert abs(m["rmse"] - 0.01 * np.sqrt(np.mean(o ** 2))) < 1e-12
+    # an orthogonal error of equal norm: 1 - cos = 1 - 1/sqrt(2) in that row
+    v = np.zeros((1, 4))
+    v[0, 0] = 1.0
+    w = np.zeros((1, 4))
+    w[0, :2] = 1.0
+    m2 = check.metrics(w, np.zeros(1), v, np.zeros(1))
+    assert abs(m2["one_minus_cos"] - (1 - 1 / np.sqrt(2))) < 1e-12
