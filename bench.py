@@ -10,13 +10,17 @@ Default workload: 64-head MLA decode, batch 64, one query token, ragged context
 lengths uniform in [8192, 32768], 64-token pages in shuffled physical order.
 
 `value` is the achieved KV-cache read rate, sum of context lengths x 644 B per
-token / step time, over K back-to-back steps after W warm-up steps.  Also
-reported: the same step captured once as a HIP graph and replayed (no faster
-here: the eager launches overlap their gaps), cold-cache step times (a 1 GiB
-scratch write and read between steps, outside the timed region: the read
-leaves the caches clean, so no write-back of scratch lines lands inside the
-step), the per-call split, the roofline of the decode call and the CPU oracle
-on a bounded sample.
+token / step time, over K back-to-back steps after W warm-up steps, with the QK
+content term on the FP8 matrix cores (the default mode).  Also reported: the
+same step in the exact-accumulation QK mode (SNAPMLA_DECODE_EXACT_QK) on the same
+cache; the step captured once as a HIP graph and replayed; cold-cache step times
+(a 1 GiB scratch write and read between steps, outside the timed region: the
+read leaves the caches clean, so no write-back of scratch lines lands inside the
+step); the per-call split; the roofline of the decode call, with two measured
+reference rates beside the 8 TB/s peak (the decode's own copy structure without
+arithmetic, and a plain 16-byte-load read stream over as many bytes); the error
+of both QK modes against an unquantized reference (fp32 attention on the bf16
+inputs) on sampled sequences; and the CPU oracle on a bounded sample.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -525,6 +529,66 @@ def read_ceiling(run, w, timed, units=256, reps=50):
             "GBps": round(page_bytes / (ms * 1e-3) / 1e9, 1)}
 
 
+def plain_stream(nbytes, timed, grid=2048, reps=20):
+    """Time snapmla_debug_read_stream over a buffer of `nbytes` (the KV bytes of the workload): the
+    plain 16-byte-load read stream, the memory system's rate for the simplest streaming kernel."""
+    import torch
+    from paper_2602_10718_amd import snapmla as sm
+    n = (nbytes + 15) // 16 * 16
+    buf = torch.ones(n // 4, dtype=torch.int32, device="cuda")
+    out = torch.empty(grid, dtype=torch.int32, device="cuda")
+
+    def call():
+        sm.snapmla_debug_read_stream(buf, grid, out)
+    for _ in range(5):
+        call()
+    ms = timed(call, reps)
+    del buf
+    return {"kernel": "read_stream_kernel (snapmla_debug_read_stream), HIP events", "grid": grid, "bytes": n,
+            "us": round(ms * 1e3, 1), "GBps": round(n / (ms * 1e-3) / 1e9, 1)}
+
+
+def accuracy_vs_bf16(run, w, samples=8):
+    """Error of the step's output against an unquantized reference: fp32 softmax attention on the same
+    bf16 inputs (plain torch on the GPU), over `samples` sequences spread over the batch.  The decode is
+    merged into a float32 output so that the figure is the kernel's, not the output rounding's."""
+    import numpy as np
+    import torch
+    from paper_2602_10718_amd import snapmla as sm
+    out32 = torch.empty((w.B, w.q_len, w.H, 512), dtype=torch.float32, device="cuda")
+    lse32 = torch.empty((w.B, w.q_len, w.H), dtype=torch.float32, device="cuda")
+    run.append_decode()
+    sm.snapmla_combine(run.workspace, run.seq_lens, w.B, w.q_len, w.H, run.num_splits, run.kv_chunk_tokens, out32,
+                       lse32)
+    torch.cuda.synchronize()
+    picks = sorted(set(np.linspace(0, w.B - 1, min(samples, w.B)).round().astype(int).tolist()))
+    num = den = sse = 0.0
+    cos_sum, rows, worst = 0.0, 0, 0.0
+    for b in picks:
+        N = int(w.seq_lens[b])
+        if N == 0:
+            continue
+        ck, kr = w.tokens(b, 0, N)
+        c = torch.from_numpy(ck.view(np.int16)).cuda().view(torch.bfloat16)
+        k = torch.from_numpy(kr.view(np.int16)).cuda().view(torch.bfloat16)
+        vis = [N - w.q_len + 1 + t if w.causal else N for t in range(w.q_len) for _ in range(w.H)]
+        ref = torch_attention_f32(run.q_nope[b].reshape(-1, 512), run.q_rope[b].reshape(-1, 64), c, k, w.tau,
+                                  vis).double()
+        o = out32[b].reshape(-1, 512).double()
+        d = o - ref
+        num += float(torch.sum(d * d))
+        den += float(torch.sum(ref * ref))
+        cos = torch.sum(o * ref, dim=1) / (torch.linalg.norm(o, dim=1) * torch.linalg.norm(ref, dim=1))
+        cos_sum += float(torch.sum(1 - cos))
+        rows += o.shape[0]
+        worst = max(worst, float(torch.max(torch.max(torch.abs(d), dim=1).values
+                                           / torch.clamp(torch.max(torch.abs(ref), dim=1).values, min=1.0))))
+    return {"reference": "fp32 softmax attention on the bf16 inputs (torch on the GPU), float32 merge output",
+            "sequences": picks, "rows": rows, "rel_l2": float(np.sqrt(num / den)),
+            "rmse": float(np.sqrt(num / (rows * 512))), "one_minus_cos": cos_sum / rows,
+            "max_abs_over_row_scale": worst}
+
+
 def wl_describe(name):
     from paper_2602_10718_amd import workloads as wl
     return wl.describe(name)
@@ -663,9 +727,26 @@ def main():
                 "median_GBps": round(kv_bytes / (float(np.median(ts)) * 1e-6) / 1e9, 1)}
         _log(f"cold: median {cold['median_us']} us, p90 {cold['p90_us']} us")
 
+    # ---- the exact-accumulation QK mode, same cache, same plan ----------------
+    run_x = DecodeRunner(w, num_splits=run.num_splits, out_dtype=torch.bfloat16,
+                         cache=(run.kv_latent, run.kv_scale, run.k_rope), exact_qk=True)
+    for _ in range(args.warmup):
+        run_x.step()
+    torch.cuda.synchronize()
+    exact_ms = timed(run_x.step, args.steps)
+    exact_dec_us = timed(run_x.append_decode, args.steps) * 1e3
+    _log(f"exact-QK mode: {exact_ms * 1e3:.1f} us/step, append_decode {exact_dec_us:.1f} us")
+
     # ---- read-stream ceiling over the same pages (a measurement kernel) --------
     ceiling = read_ceiling(run, w, timed)
     _log(f"read-stream ceiling: {ceiling['us']} us, {ceiling['GBps']} GB/s of whole pages")
+    stream_ref = plain_stream(kv_bytes, timed)
+    _log(f"plain read stream: {stream_ref['us']} us, {stream_ref['GBps']} GB/s")
+
+    # ---- error against the unquantized (bf16-input, fp32) reference -----------
+    acc = {"fp8_qk": accuracy_vs_bf16(run, w), "exact_qk": accuracy_vs_bf16(run_x, w)}
+    _log(f"vs bf16 reference: rel_l2 {acc['fp8_qk']['rel_l2']:.3e} (FP8 QK), {acc['exact_qk']['rel_l2']:.3e} (exact QK)")
+    del run_x
 
     gbps = kv_bytes / (ms_per_step * 1e-3) / 1e9
     decode_gbps = kv_bytes / (decode_us * 1e-6) / 1e9
@@ -689,6 +770,8 @@ def main():
                     "unit": "GB/s", "frac": round(decode_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                     "algorithmic_bytes_per_launch": kv_bytes}
     roofline["read_ceiling"] = ceiling
+    stream_ref["decode_call_frac"] = round(stream_ref["us"] / decode_us, 4)
+    roofline["plain_stream"] = stream_ref
     line = {
         "metric": METRIC,
         "value": round(gbps, 1),
@@ -718,6 +801,11 @@ def main():
         "warm_step_us_each": {"steps": args.steps, "median": round(float(np.median(step_each)), 1),
                               "p90": round(float(np.percentile(step_each, 90)), 1)},
         "cold_cache": cold,
+        "qk_mode": "FP8 matrix cores (flags 0)",
+        "exact_qk": {"flags": "SNAPMLA_DECODE_EXACT_QK", "us_per_step": round(exact_ms * 1e3, 1),
+                     "GBps": round(kv_bytes / (exact_ms * 1e-3) / 1e9, 1),
+                     "append_decode_us": round(exact_dec_us, 1)},
+        "accuracy_vs_bf16": acc,
         "roofline": roofline,
         "cache_fill_s": round(t_fill, 1),
     }

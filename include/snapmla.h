@@ -332,6 +332,20 @@ int snapmla_debug_read_ceiling(const uint8_t* kv_latent, const float* kv_scale, 
                                uint32_t* out, hipStream_t stream);
 
 /*
+ * snapmla_debug_read_stream -- measurement only: `bytes` of device memory read
+ * once by the simplest streaming kernel (16-byte vector loads, grid-stride loop,
+ * consecutive lanes on consecutive words, `grid` workgroups of 256 threads).
+ * Its duration is the plain read-stream rate of the memory system, the second
+ * reference figure (beside the 8 TB/s peak) for the decode's bandwidth.
+ *   buf    device, read; 16-byte aligned; bytes a multiple of 16, >= 0
+ *   grid   1 .. 2^20 workgroups
+ *   out    uint32 [grid] (device, written): per workgroup, the XOR of every
+ *          dword it read (workgroup g reads the 16-byte words i with
+ *          (i / 256) % grid == g), so a test can check the reads
+ */
+int snapmla_debug_read_stream(const void* buf, int64_t bytes, int32_t grid, uint32_t* out, hipStream_t stream);
+
+/*
  * snapmla_debug_mfma_fp8 -- test hook: the FP8 matrix-core dot product the decode's
  * QK content term is formed with (Section 3.1 runs that GEMM on FP8 matrix
  * cores).  For every tile t, one 16x16x128 FP8 MFMA from a zero accumulator:

@@ -434,3 +434,13 @@ int snapmla_debug_read_ceiling(const uint8_t* kv_latent, const float* kv_scale, 
   a.units = units;
   return hip_status(snapmla::launch_read_ceiling(a, stream), "read_ceiling launch");
 }
+
+int snapmla_debug_read_stream(const void* buf, int64_t bytes, int32_t grid, uint32_t* out, hipStream_t stream) {
+  if (bytes < 0 || bytes % 16 != 0)
+    return fail(SNAPMLA_INVALID_ARGUMENT, "bytes must be a non-negative multiple of 16 (got %lld)", (long long)bytes);
+  if (grid < 1 || grid > (1 << 20)) return fail(SNAPMLA_INVALID_ARGUMENT, "grid must be in [1, 2^20] (got %d)", grid);
+  if (!out || (bytes > 0 && !buf)) return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer");
+  if (misaligned(buf)) return fail(SNAPMLA_MISALIGNED, "buf must be 16-byte aligned");
+  if (misaligned4(out)) return fail(SNAPMLA_MISALIGNED, "out must be 4-byte aligned");
+  return hip_status(snapmla::launch_read_stream(buf, bytes / 16, grid, out, stream), "read_stream launch");
+}

@@ -115,3 +115,37 @@ hipError_t launch_read_ceiling(const CeilingArgs& a, hipStream_t stream) {
 }
 
 }  // namespace snapmla
+
+namespace snapmla {
+
+// Plain read stream (a measurement kernel): the buffer read once with 16-byte
+// vector loads, a grid-stride loop over 16-byte words with consecutive lanes on
+// consecutive words, each thread XOR-folding what it read; each workgroup
+// writes the XOR of its 256 threads.  No LDS, no copies: the rate the memory
+// system gives a simple streaming kernel, the second reference figure beside
+// the 8 TB/s peak.
+__global__ __launch_bounds__(256) void read_stream_kernel(const v4i* __restrict__ p, int64_t n16, uint32_t* out) {
+  __shared__ uint32_t red[4];
+  v4i acc = {0, 0, 0, 0};
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride) acc ^= p[i];
+  uint32_t x = (uint32_t)(acc[0] ^ acc[1] ^ acc[2] ^ acc[3]);
+  x ^= __shfl_xor(x, 32);
+  x ^= __shfl_xor(x, 16);
+  x ^= __shfl_xor(x, 8);
+  x ^= __shfl_xor(x, 4);
+  x ^= __shfl_xor(x, 2);
+  x ^= __shfl_xor(x, 1);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) out[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
+hipError_t launch_read_stream(const void* buf, int64_t n16, int grid, uint32_t* out, hipStream_t stream) {
+  if (grid <= 0) return hipSuccess;
+  hipLaunchKernelGGL(read_stream_kernel, dim3((unsigned)grid), dim3(256), 0, stream,
+                     static_cast<const v4i*>(buf), n16, out);
+  return hipGetLastError();
+}
+
+}  // namespace snapmla

@@ -133,5 +133,7 @@ struct CeilingArgs {
   int nblk, num_pages, units;
 };
 hipError_t launch_read_ceiling(const CeilingArgs& a, hipStream_t stream);
+// Plain read stream (measurement): n16 16-byte words read by `grid` workgroups of 256 threads.
+hipError_t launch_read_stream(const void* buf, int64_t n16, int grid, uint32_t* out, hipStream_t stream);
 
 }  // namespace snapmla

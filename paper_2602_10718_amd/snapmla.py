@@ -66,12 +66,14 @@ lib.snapmla_debug_mfma_fp8.argtypes = [_p, _p, _p, _i64, _p]
 lib.snapmla_debug_set_spin_limit.restype = ctypes.c_int
 lib.snapmla_debug_set_spin_limit.argtypes = [_i32]
 lib.snapmla_debug_read_ceiling.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p]
+lib.snapmla_debug_read_stream.restype = ctypes.c_int
+lib.snapmla_debug_read_stream.argtypes = [_p, _i64, _i32, _p, _p]
 
 EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_append", "snapmla_quantize_rows",
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
            "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16",
            "snapmla_debug_read_ceiling", "snapmla_append_decode", "snapmla_debug_set_spin_limit",
-           "snapmla_debug_mfma_fp8"]
+           "snapmla_debug_mfma_fp8", "snapmla_debug_read_stream"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -124,6 +126,13 @@ def snapmla_quantize_append(c_kv_new, k_rope_new, page_table, seq_lens, num_page
 def snapmla_quantize_rows(x, codes, scale, stream=None):
     """x bf16 [rows, 512] -> codes uint8 [rows, 512], scale f32 [rows]."""
     _check(lib.snapmla_quantize_rows(_ptr(x), x.numel() // 512, _ptr(codes), _ptr(scale), _stream(stream)))
+
+
+def snapmla_debug_read_stream(buf, grid, out, stream=None):
+    """Measurement hook: read the whole of `buf` (a device tensor, 16-byte multiple) once with plain
+    16-byte vector loads by `grid` workgroups; `out` int32 [grid] receives per-workgroup XOR checksums."""
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib.snapmla_debug_read_stream(_ptr(buf), nbytes, grid, _ptr(out), _stream(stream)))
 
 
 def snapmla_debug_read_ceiling(kv_latent, kv_scale, k_rope, pages, num_pages, units, out, stream=None):

@@ -158,6 +158,17 @@ def test_read_ceiling_validates(sm):
     assert L.snapmla_debug_read_ceiling(4096, 4096, 4096, 4098, 10, 4, 1, 4096, None) == 4        # misaligned pages
 
 
+def test_read_stream_validates(sm):
+    L = sm.lib
+    assert L.snapmla_debug_read_stream(4096, -16, 4, 4096, None) == 1        # bytes < 0
+    assert L.snapmla_debug_read_stream(4096, 24, 4, 4096, None) == 1         # not a multiple of 16
+    assert L.snapmla_debug_read_stream(4096, 64, 0, 4096, None) == 1         # grid < 1
+    assert L.snapmla_debug_read_stream(None, 64, 4, 4096, None) == 1         # null buffer
+    assert L.snapmla_debug_read_stream(4096, 64, 4, None, None) == 1         # null out
+    assert L.snapmla_debug_read_stream(4104, 64, 4, 4096, None) == 4         # misaligned buffer
+    assert L.snapmla_debug_read_stream(4096, 64, 4, 4098, None) == 4         # misaligned out
+
+
 
 def test_append_decode_validates(sm):
     L = sm.lib

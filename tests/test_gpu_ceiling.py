@@ -1,4 +1,5 @@
-"""GPU: the read-stream ceiling kernel (snapmla_debug_read_ceiling) reads every listed page.
+"""GPU: the read-stream ceiling kernel (snapmla_debug_read_ceiling) reads every listed page, and the
+plain read stream (snapmla_debug_read_stream) reads every word of its buffer.
 
 The kernel is a measurement tool: it streams pages into LDS with the decode's copy
 structure and folds the first KiB of every latent and RoPE page into a per-unit XOR.
@@ -67,3 +68,20 @@ def test_out_of_range_ids_read_page_zero_and_empty_list():
     assert np.array_equal(got, _expected(lat, rope, pages, 2, P))
     empty = _run(lat, sc, rope, np.zeros(0, np.int32), 3)
     assert np.array_equal(empty, np.zeros(3, np.uint32))
+
+
+@pytest.mark.parametrize("words,grid", [(1, 1), (1000, 3), (256 * 7 + 5, 2), (1 << 18, 64)])
+def test_plain_stream_checksums(words, grid):
+    rng = np.random.default_rng(words + grid)
+    buf = rng.integers(0, 1 << 32, (words, 4), dtype=np.uint32)
+    out = torch.full((grid,), -1, dtype=torch.int32, device="cuda")
+    print(f"[read_stream] words={words} grid={grid}", flush=True)
+    sm.snapmla_debug_read_stream(torch.from_numpy(buf.view(np.int32)).cuda(), grid, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32)
+    # thread t of workgroup g reads words (g + grid * j) * 256 + t
+    owner = (np.arange(words) // 256) % grid
+    folded = np.bitwise_xor.reduce(buf, axis=1)
+    exp = np.array([np.bitwise_xor.reduce(folded[owner == g]) if np.any(owner == g) else 0 for g in range(grid)],
+                   np.uint32)
+    assert np.array_equal(got, exp)
