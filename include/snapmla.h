@@ -202,6 +202,40 @@ int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t 
                           void* workspace, size_t workspace_bytes,
                           hipStream_t stream);
 
+/* Bytes of the static scratch of snapmla_append_decode_noalloc (128 MiB per GPU). */
+#define SNAPMLA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/*
+ * snapmla_append_decode_noalloc -- for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops or harnesses that forbid
+ * hipMalloc): the whole step of snapmla_append_decode followed by
+ * snapmla_combine, with the workspace in a static array inside the library
+ * instead of a caller buffer.  Same results as those two calls with a caller
+ * workspace, bit for bit; allocates nothing (the array is part of the library's
+ * device code: every GPU the library runs on holds its own 128 MiB copy until
+ * the process ends; its device address is looked up once per device, on the
+ * first call with that device current).
+ *   arguments as snapmla_append_decode, without workspace/workspace_bytes, and
+ *   out, out_dtype, lse as snapmla_combine
+ *   the plan's workspace (snapmla_decode_workspace_size) must fit in
+ *   SNAPMLA_NOALLOC_SCRATCH_BYTES, else SNAPMLA_WORKSPACE_TOO_SMALL and nothing
+ *   is enqueued (a 64-row group per 256 split parts needs ~40 MiB)
+ * Every call on one GPU uses that GPU's one array, and nothing in it is assumed
+ * to start at zero (each call writes what it reads).  Calls that overlap on one
+ * GPU (other streams, other threads, without ordering between them) race on the
+ * array and give wrong results: order them on one stream or with events.
+ */
+int snapmla_append_decode_noalloc(const void* c_kv_new, const void* k_rope_new, int32_t n_new,
+                                  const void* q_nope, const void* q_rope,
+                                  uint8_t* kv_latent, float* kv_scale, void* k_rope,
+                                  const int32_t* page_table, const int32_t* seq_lens,
+                                  int32_t B, int32_t q_len, int32_t H,
+                                  int32_t max_pages, int32_t num_pages, int32_t page_size,
+                                  float softmax_scale, int32_t causal,
+                                  int32_t num_splits, int32_t kv_chunk_tokens, int32_t flags,
+                                  void* out, int32_t out_dtype, float* lse,
+                                  hipStream_t stream);
+
 /*
  * snapmla_decode_bf16 -- the BF16-cache baseline of the paper's comparison
  * (Section 4: the FP8 kernel against MLA decode over a BF16 cache).  Same

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "snapmla.h"
@@ -443,4 +444,69 @@ int snapmla_debug_read_stream(const void* buf, int64_t bytes, int32_t grid, uint
   if (misaligned(buf)) return fail(SNAPMLA_MISALIGNED, "buf must be 16-byte aligned");
   if (misaligned4(out)) return fail(SNAPMLA_MISALIGNED, "out must be 4-byte aligned");
   return hip_status(snapmla::launch_read_stream(buf, bytes / 16, grid, out, stream), "read_stream launch");
+}
+
+// ---- the decode step without a caller workspace ------------------------------
+// snapmla_append_decode_noalloc keeps its workspace in this file-scope array
+// (each GPU the library runs on holds its own copy until the process ends).  In
+// host code `scratch` only names the array: its device address on the current
+// GPU comes from hipGetSymbolAddress, taken once per device and cached below,
+// and only that address is handed to kernels.
+static __device__ __align__(256) uint8_t scratch[SNAPMLA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_addr[kMaxDevices] = {};   // device address of `scratch` per device, null until resolved
+
+int scratch_address(void** addr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(SNAPMLA_UNSUPPORTED, "device %d is beyond the %d devices the scratch table holds", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_addr[dev]) {
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!a) return fail(SNAPMLA_HIP_ERROR, "hipGetSymbolAddress(scratch) gave a null address");
+    g_scratch_addr[dev] = a;
+  }
+  *addr = g_scratch_addr[dev];
+  return SNAPMLA_OK;
+}
+
+}  // namespace
+
+int snapmla_append_decode_noalloc(const void* c_kv_new, const void* k_rope_new, int32_t n_new, const void* q_nope,
+                                  const void* q_rope, uint8_t* kv_latent, float* kv_scale, void* k_rope,
+                                  const int32_t* page_table, const int32_t* seq_lens, int32_t B, int32_t q_len,
+                                  int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
+                                  float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
+                                  int32_t flags, void* out, int32_t out_dtype, float* lse, hipStream_t stream) {
+  int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
+  if (st != SNAPMLA_OK) return st;
+  const size_t need = snapmla::ws_layout(B, q_len, H, num_splits, kv_chunk_tokens).total;
+  if (need > SNAPMLA_NOALLOC_SCRATCH_BYTES)
+    return fail(SNAPMLA_WORKSPACE_TOO_SMALL,
+                "this call needs %zu bytes of workspace; the static scratch holds %zu (fewer splits or rows per "
+                "call, or snapmla_append_decode with a caller workspace)",
+                need, (size_t)SNAPMLA_NOALLOC_SCRATCH_BYTES);
+  if (out_dtype != 0 && out_dtype != 1) return fail(SNAPMLA_INVALID_ARGUMENT, "out_dtype must be 0 or 1");
+  if (n_new < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "n_new must be >= 0 (got %d)", n_new);
+  if (B == 0) return ok();
+  if (!out) return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
+  if (misaligned(out) || (lse && misaligned4(lse)))
+    return fail(SNAPMLA_MISALIGNED, "out must be 16-byte aligned, lse 4-byte aligned");
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != SNAPMLA_OK) return st;
+  st = snapmla_append_decode(c_kv_new, k_rope_new, n_new, q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table,
+                             seq_lens, B, q_len, H, max_pages, num_pages, page_size, softmax_scale, causal,
+                             num_splits, kv_chunk_tokens, flags, ws, SNAPMLA_NOALLOC_SCRATCH_BYTES, stream);
+  if (st != SNAPMLA_OK) return st;
+  return snapmla_combine(ws, SNAPMLA_NOALLOC_SCRATCH_BYTES, seq_lens, B, q_len, H, num_splits, kv_chunk_tokens, out,
+                         out_dtype, lse, stream);
 }

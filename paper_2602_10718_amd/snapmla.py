@@ -66,6 +66,9 @@ lib.snapmla_debug_mfma_fp8.argtypes = [_p, _p, _p, _i64, _p]
 lib.snapmla_debug_set_spin_limit.restype = ctypes.c_int
 lib.snapmla_debug_set_spin_limit.argtypes = [_i32]
 lib.snapmla_debug_read_ceiling.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p]
+lib.snapmla_append_decode_noalloc.restype = ctypes.c_int
+lib.snapmla_append_decode_noalloc.argtypes = [_p, _p, _i32, _p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32,
+                                              _i32, ctypes.c_float, _i32, _i32, _i32, _i32, _p, _i32, _p, _p]
 lib.snapmla_debug_read_stream.restype = ctypes.c_int
 lib.snapmla_debug_read_stream.argtypes = [_p, _i64, _i32, _p, _p]
 
@@ -73,7 +76,7 @@ EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_ap
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
            "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16",
            "snapmla_debug_read_ceiling", "snapmla_append_decode", "snapmla_debug_set_spin_limit",
-           "snapmla_debug_mfma_fp8", "snapmla_debug_read_stream"]
+           "snapmla_debug_mfma_fp8", "snapmla_debug_read_stream", "snapmla_append_decode_noalloc"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -179,6 +182,32 @@ def snapmla_append_decode(c_kv_new, k_rope_new, q_nope, q_rope, kv_latent, kv_sc
                                      B, q_len, H, page_table.shape[1], kv_latent.shape[0], page_size,
                                      float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, int(flags),
                                      _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20   # SNAPMLA_NOALLOC_SCRATCH_BYTES
+
+
+def snapmla_append_decode_noalloc(c_kv_new, k_rope_new, q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table,
+                                  seq_lens, softmax_scale, causal, num_splits, kv_chunk_tokens, out, lse=None,
+                                  page_size=64, stream=None, flags=0):
+    """snapmla_append_decode + snapmla_combine with the workspace in the library's static scratch (for callers
+    that cannot allocate); out bf16 or f32 [B, q_len, H, 512], lse f32 [B, q_len, H] or None."""
+    B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
+    n_new = c_kv_new.shape[1]
+    _check(lib.snapmla_append_decode_noalloc(_ptr(c_kv_new), _ptr(k_rope_new), n_new, _ptr(q_nope), _ptr(q_rope),
+                                             _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope), _ptr(page_table),
+                                             _ptr(seq_lens), B, q_len, H, page_table.shape[1], kv_latent.shape[0],
+                                             page_size, float(softmax_scale), int(causal), num_splits,
+                                             kv_chunk_tokens, int(flags), _ptr(out), _out_dtype(out), _ptr(lse),
+                                             _stream(stream)))
+
+
+def _out_dtype(out):
+    if out.dtype == torch.float32:
+        return 1
+    if out.dtype == torch.bfloat16:
+        return 0
+    raise ValueError("out must be bfloat16 or float32")
 
 
 def snapmla_combine(workspace, seq_lens, B, q_len, H, num_splits, kv_chunk_tokens, out, lse=None, stream=None):
