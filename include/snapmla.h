@@ -400,7 +400,7 @@ int snapmla_debug_mfma_fp8(const uint8_t* a, const uint8_t* b, float* c, int64_t
  * 4194304).  The waits end by construction; the bound only guarantees that a
  * kernel terminates.  A wait that reaches it marks its KV piece, whose outputs
  * and LSEs then come out NaN, so a lost handshake is visible rather than
- * silently stale.  With polls = 0 every wait gives up at once (every output
+ * silently stale.  With polls = 0 every wait gives up after its first poll (every output
  * NaN), which lets a test check that path without hanging anything.
  *   polls >= 0 (SNAPMLA_INVALID_ARGUMENT otherwise).  Process-wide; not for
  *   concurrent use with decode calls on other threads.

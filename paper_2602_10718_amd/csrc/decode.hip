@@ -120,6 +120,8 @@ __device__ __forceinline__ int flag_load(const int* f) {
 // would become a flat load, which queues behind the page copies).
 typedef __attribute__((address_space(3))) volatile v4i lds_flags4;
 __device__ __forceinline__ v4i flag_load4(const int* f) { return *(const lds_flags4*)(f); }
+// all four QK waves have published block k
+__device__ __forceinline__ bool flags_past(v4i f4, int k) { return f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k; }
 
 template <bool kRotate, bool kExact>
 __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int32_t* __restrict__ prefix,
@@ -637,12 +639,15 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         }
         // codes and state of block k, once all four QK waves have published them
         {
+          // one exit for both ends of the wait (the flags seen, or the bound reached),
+          // decided again from the last poll: codes never published, or a zero
+          // bound, mark the piece, which then comes out NaN
+          v4i f4;
           int spin = 0;
-          for (; spin < a.spin_limit; ++spin) {
-            const v4i f4 = flag_load4(xf);
-            if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
-          }
-          if (spin == a.spin_limit) cur_bad = true;   // codes never published: the piece comes out NaN
+          do {
+            f4 = flag_load4(xf);
+          } while (!flags_past(f4, k) && ++spin < a.spin_limit);
+          if (!flags_past(f4, k) || a.spin_limit <= 0) cur_bad = true;
         }
         asm volatile("" ::: "memory");
         gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
@@ -800,12 +805,15 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         if (!RD) return false;
         // codes and state of block k, once all four QK waves have published them
         {
+          // one exit for both ends of the wait (the flags seen, or the bound reached),
+          // decided again from the last poll: codes never published, or a zero
+          // bound, mark the piece, which then comes out NaN
+          v4i f4;
           int spin = 0;
-          for (; spin < a.spin_limit; ++spin) {
-            const v4i f4 = flag_load4(xf);
-            if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
-          }
-          if (spin == a.spin_limit) cur_bad = true;   // codes never published: the piece comes out NaN
+          do {
+            f4 = flag_load4(xf);
+          } while (!flags_past(f4, k) && ++spin < a.spin_limit);
+          if (!flags_past(f4, k) || a.spin_limit <= 0) cur_bad = true;
         }
         asm volatile("" ::: "memory");
         gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);

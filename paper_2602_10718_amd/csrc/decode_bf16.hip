@@ -405,12 +405,14 @@ __global__ __launch_bounds__(512, 1) void decode_bf16_kernel(DecodeArgs a, const
         }
       }
       {
+        // one exit for both ends of the wait, decided again from the last poll: codes
+        // never published, or a zero bound, mark the piece, which then comes out NaN
+        v4i f4;
         int spin = 0;
-        for (; spin < a.spin_limit; ++spin) {
-          const v4i f4 = fload4(xf);
-          if (f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) break;
-        }
-        if (spin == a.spin_limit) cur_bad = true;   // codes never published: the piece comes out NaN
+        do {
+          f4 = fload4(xf);
+        } while (!(f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) && ++spin < a.spin_limit);
+        if (!(f4[0] > k && f4[1] > k && f4[2] > k && f4[3] > k) || a.spin_limit <= 0) cur_bad = true;
       }
       asm volatile("" ::: "memory");
       gl0 = *reinterpret_cast<const v4f*>(xg + n * 4);
