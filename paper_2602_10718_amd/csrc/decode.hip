@@ -93,6 +93,13 @@ constexpr float kLn2 = 0.69314718055994531f;
 constexpr int kPieceStores = 2 * (16 + 1);
 static_assert(20 + kPieceStores < 64, "wait counter range");
 
+// Branch weights for the block layout: the rare cases of a period (a piece start
+// or end, a sequence's last page, the first and last periods) are laid out off the
+// straight path, which then runs with fewer taken branches.
+// (macros: the hint must sit in the branch condition itself to reach the layout)
+#define likely(c) __builtin_expect(!!(c), 1)
+#define unlikely(c) __builtin_expect(!!(c), 0)
+
 // Latent rows are stored with 16-byte chunk c of token t at chunk c ^ swz(t),
 // RoPE rows with chunk c at c ^ rswz(t).  Sixteen consecutive tokens (the QK
 // operand reads) map a given chunk to sixteen distinct 16-byte bank groups, and
@@ -264,7 +271,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     for (int k = 0; k < nblocks; ++k) {
       barrier_vm_lgkm0<63>();                              // page k has landed (PV waves waited)
       const int gb = gstart + k;
-      if (gb >= cur_end) {                                 // first block of a later piece
+      if (unlikely(gb >= cur_end)) {                                 // first block of a later piece
         if (!q_ready) {
           if (!nx_ready) fetch_next(gb);
           load_q(nx_b);
@@ -343,7 +350,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         }
       }
       const bool tail = (blk + 1) * kPage > vis;   // some token of this block is hidden from this row
-      if (tail) {
+      if (unlikely(tail)) {
         // hidden tokens and stale slots past the sequence end: logit -inf, scale 0
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
@@ -359,7 +366,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       const float mb = quad_max(mt) * sl2;         // block max of this row (log2 units)
       v4i mine = v4i{0, 0, 0, 0};
       float gam = 1.0f;
-      if (mb > -INFINITY) {                        // the row sees a token of this block
+      if (likely(mb > -INFINITY)) {                        // the row sees a token of this block
         const float m_new = fmaxf(m, mb);
         float e[16];
 #pragma unroll
@@ -395,7 +402,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       if (g4 == 0) *reinterpret_cast<v4f*>(xg + (16 * w + n16) * 4) = v4f{gam, l, m, sp};
       lds_wait_all();
       if (lane == 0) flag_store(xf + w, k + 1);   // block k published
-      if (cur_end < gend) {                        // a later piece starts inside the range
+      if (unlikely(cur_end < gend)) {                        // a later piece starts inside the range
         if (!nx_ready && gb + 2 >= cur_end) {
           fetch_next(cur_end);
           nx_ready = true;
@@ -431,7 +438,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
     int ib = cur_b, ib_lo = cur_p0, ib_hi = cur_end;
     auto page_entry = [&](int kb) -> const int32_t* {
       const int gb = gstart + min(kb, nblocks - 1);
-      while (gb >= ib_hi) {                        // skips sequences without blocks
+      while (unlikely(gb >= ib_hi)) {                        // skips sequences without blocks
         ++ib;
         ib_lo = ib_hi;
         ib_hi = prefix[ib + 1];
@@ -530,9 +537,9 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       // requests, so "at most 20 (+ kPieceStores) outstanding" suffices; 19 in
       // period 0, after the prologue.
       auto top_barrier = [&](int k, bool after_stores) {
-        if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
-        else if (k == 0) barrier_vm_lgkm0<19>();
-        else if (after_stores) barrier_vm_lgkm0<20 + kPieceStores>();
+        if (unlikely(k + 1 >= nblocks)) barrier_vm_lgkm0<0>();
+        else if (unlikely(k == 0)) barrier_vm_lgkm0<19>();
+        else if (unlikely(after_stores)) barrier_vm_lgkm0<20 + kPieceStores>();
         else barrier_vm_lgkm0<20>();
       };
 
@@ -544,7 +551,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       for (int k = 0;; ++k) {
         top_barrier(k, stored);
         stored = false;
-        if (k > 0) {
+        if (likely(k > 0)) {
           // ---- PV of block k-1 --------------------------------------------------
   #pragma unroll
           for (int T = 0; T < 4; ++T) {
@@ -560,7 +567,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           }
           // ---- end of a piece: write the normalized partial output and LSE ----
           // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
-          if (k == nblocks || gstart + k >= cur_end) {
+          if (unlikely(k == nblocks || gstart + k >= cur_end)) {
             const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
                                                     : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
             const float nanv = __builtin_nanf("");
@@ -601,17 +608,17 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         }
         // copies after the products and the piece-end stores, so that the stores
         // precede the period's copies in the wait counter
-        if (k + 2 < nblocks) {
+        if (likely(k + 2 < nblocks)) {
           request_page(k + 6);
           copy_rope_scale(k + 2, pg_rope);
           copy_latent(k + 3, pg_lat);
           pg_rope = pg_lat;
         }
-        if (k == nblocks) break;
+        if (unlikely(k == nblocks)) break;
 
         // ---- block k: piece bookkeeping (mirrors the QK waves) -----------------
         const int gb = gstart + k;
-        if (gb >= cur_end) {
+        if (unlikely(gb >= cur_end)) {
           fetch_next(gb);
           take_next(gb);
           cur_bad = false;
@@ -619,7 +626,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         cur_bad |= ((stage_bad >> (k % kLatStages)) & 1u) != 0;
         const int valid = min(kPage, cur_n - (gb - cur_p0) * kPage);
         uint8_t* stp = smem + (k % kLatStages) * kLatBytes;
-        if (valid < kPage) {
+        if (unlikely(valid < kPage)) {
           // last page of a sequence: clear the bytes of the slots past its end that
           // this wave reads (stale data could hold NaN codes; their probability
           // codes are 0).  The QK waves mask these slots whatever they hold.
@@ -675,9 +682,9 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
       // outstanding" suffices (capped at the counter's range, which only waits
       // longer); 19 in period 0, after the prologue.
       auto top_barrier = [&](int k, int storing_periods) {
-        if (k + 1 >= nblocks) barrier_vm_lgkm0<0>();
-        else if (k == 0) barrier_vm_lgkm0<19>();
-        else if (storing_periods == 0) barrier_vm_lgkm0<20>();
+        if (unlikely(k + 1 >= nblocks)) barrier_vm_lgkm0<0>();
+        else if (unlikely(k == 0)) barrier_vm_lgkm0<19>();
+        else if (likely(storing_periods == 0)) barrier_vm_lgkm0<20>();
         else if (storing_periods == 1) barrier_vm_lgkm0<20 + kPieceStores>();
         else barrier_vm_lgkm0<63>();
       };
@@ -698,7 +705,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         top_barrier(k, (st1 ? 1 : 0) + (st2 ? 1 : 0));
         st2 = st1;
         st1 = false;
-        if (k + 2 < nblocks) {
+        if (likely(k + 2 < nblocks)) {
           request_page(k + 6);
           copy_rope_scale(k + 2, pg_rope);
           copy_latent(k + 3, pg_lat);
@@ -712,7 +719,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         if (RD) {
           // ---- block k: piece bookkeeping (mirrors the QK waves) ---------------
           const int gb = gstart + k;
-          if (gb >= cur_end) {
+          if (unlikely(gb >= cur_end)) {
             fetch_next(gb);
             take_next(gb);
             cur_bad = false;
@@ -720,7 +727,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           cur_bad |= ((stage_bad >> (k % kLatStages)) & 1u) != 0;
           const int valid = min(kPage, cur_n - (gb - cur_p0) * kPage);
           uint8_t* stp = smem + (k % kLatStages) * kLatBytes;
-          if (valid < kPage) {
+          if (unlikely(valid < kPage)) {
             // last page of a sequence: clear the bytes of the slots past its end that
             // this wave reads (stale data could hold NaN codes; their probability
             // codes are 0).  The QK waves mask these slots whatever they hold.
@@ -765,7 +772,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         if (PV) {
           // ---- end of a piece: write the normalized partial output and LSE --
           // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
-          if (close) {
+          if (unlikely(close)) {
             const float nanv = __builtin_nanf("");
             // Exactly kPieceStores store instructions per wave, whatever R: rows up to
             // rows_pad lie inside the piece's slot (the combine reads rows < R only),
