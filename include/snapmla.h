@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define SNAPMLA_ABI_VERSION 2
+#define SNAPMLA_ABI_VERSION 3
 
 enum snapmla_status {
   SNAPMLA_OK = 0,
@@ -134,7 +134,10 @@ int snapmla_quantize_rows(const void* x, int64_t rows, uint8_t* codes, float* sc
  *                         may span several parts and a part several sequences)
  *   kv_chunk_tokens  > 0: every sequence is cut into chunks of kv_chunk_tokens
  *                         (a multiple of 64); num_splits bounds the chunks per
- *                         sequence (sequences needing more are flagged NaN)
+ *                         sequence (sequences needing more are flagged NaN).
+ *                         With kv_chunk_tokens >= max_pages*64 and num_splits == 1
+ *                         no sequence is split (the unsplit plan: one piece per
+ *                         sequence, no snapmla_combine needed when out is given)
  * *bytes receives the size; returns SNAPMLA_INVALID_ARGUMENT on bad sizes.
  */
 int snapmla_decode_workspace_size(int32_t B, int32_t q_len, int32_t H,
@@ -144,7 +147,7 @@ int snapmla_decode_workspace_size(int32_t B, int32_t q_len, int32_t H,
 /*
  * snapmla_decode -- FP8 MLA decode over the paged cache (Algorithm 1 and
  * Appendix D; Section 2 absorbed score).  Enqueues the query quantization and
- * the decode kernel; the result is complete only after snapmla_combine.
+ * the decode kernel.
  *
  * Per row r and cached token j the restored logit is
  *     s = softmax_scale * ( sigma_q[r] * sigma_K[j] * <q8_r, c8_j> + <q_rope_r, k_rope_j> )
@@ -154,8 +157,15 @@ int snapmla_decode_workspace_size(int32_t B, int32_t q_len, int32_t H,
  * p' = e * sigma_K; block scale sigma_P = max(max p' / 448, 2^-40);
  * codes pi = E4M3(p' / sigma_P); output and normalizer kept in the sigma_P
  * domain (Appendix D recurrences); the PV product pi x c8 runs in FP8.
- * Each KV piece (see snapmla_decode_workspace_size) writes its normalized
- * partial output and log-sum-exp into the workspace.
+ * A KV piece (a sequence's blocks inside one part or chunk of the split plan,
+ * see snapmla_decode_workspace_size) that covers its whole sequence writes the
+ * final rows o = O / l and LSE = m + ln(sigma_P l) (Algorithm 1 finalisation)
+ * into out and lse; the rows of sequences without blocks are written too (o = 0
+ * and LSE = -inf when empty, NaN when a data error rejects the sequence).  Every
+ * other piece writes its normalized partial output and log-sum-exp into the
+ * workspace, and snapmla_combine (same workspace, plan, out, out_dtype and lse)
+ * merges them into the remaining rows.  With out == NULL every piece writes a
+ * partial and snapmla_combine writes every row.
  *
  *   q_nope, q_rope        bf16 queries (layout above), device, read
  *   kv_latent, kv_scale, k_rope, page_table, seq_lens   cache (layout above), device, read
@@ -166,6 +176,9 @@ int snapmla_decode_workspace_size(int32_t B, int32_t q_len, int32_t H,
  *   num_splits, kv_chunk_tokens   split plan (see snapmla_decode_workspace_size)
  *   flags                 0 or SNAPMLA_DECODE_EXACT_QK (other bits: SNAPMLA_INVALID_ARGUMENT)
  *   workspace / workspace_bytes   device scratch of at least the queried size
+ *   out        [B][q_len][H][512], bf16 (out_dtype 0, round to nearest even) or
+ *              float32 (1), written; or NULL (partials only)
+ *   lse        float32 [B][q_len][H], written; may be NULL (must be NULL when out is)
  */
 int snapmla_decode(const void* q_nope, const void* q_rope,
                    const uint8_t* kv_latent, const float* kv_scale, const void* k_rope,
@@ -175,6 +188,7 @@ int snapmla_decode(const void* q_nope, const void* q_rope,
                    float softmax_scale, int32_t causal,
                    int32_t num_splits, int32_t kv_chunk_tokens, int32_t flags,
                    void* workspace, size_t workspace_bytes,
+                   void* out, int32_t out_dtype, float* lse,
                    hipStream_t stream);
 
 /*
@@ -200,6 +214,7 @@ int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t 
                           float softmax_scale, int32_t causal,
                           int32_t num_splits, int32_t kv_chunk_tokens, int32_t flags,
                           void* workspace, size_t workspace_bytes,
+                          void* out, int32_t out_dtype, float* lse,
                           hipStream_t stream);
 
 /* Bytes of the static scratch of snapmla_append_decode_noalloc (128 MiB per GPU). */
@@ -215,8 +230,8 @@ int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t 
  * device code: every GPU the library runs on holds its own 128 MiB copy until
  * the process ends; its device address is looked up once per device, on the
  * first call with that device current).
- *   arguments as snapmla_append_decode, without workspace/workspace_bytes, and
- *   out, out_dtype, lse as snapmla_combine
+ *   arguments as snapmla_append_decode, without workspace/workspace_bytes
+ *   (out must not be NULL)
  *   the plan's workspace (snapmla_decode_workspace_size) must fit in
  *   SNAPMLA_NOALLOC_SCRATCH_BYTES, else SNAPMLA_WORKSPACE_TOO_SMALL and nothing
  *   is enqueued (a 64-row group per 256 split parts needs ~40 MiB)
@@ -245,8 +260,8 @@ int snapmla_append_decode_noalloc(const void* c_kv_new, const void* k_rope_new, 
  * Per row: s = softmax_scale * (q_nope . c + q_rope . k_rope) in float32 (BF16
  * MFMA), online softmax over 32-token blocks, P rounded to bf16 for the BF16 PV
  * product (the normalizer sums the unrounded P), o = O / l, LSE = m + ln l.
- * Arguments and errors as snapmla_decode (without kv_scale); complete after
- * snapmla_combine with the same split plan.
+ * Arguments, direct rows and errors as snapmla_decode (without kv_scale); the
+ * other rows are complete after snapmla_combine with the same split plan.
  */
 int snapmla_decode_bf16(const void* q_nope, const void* q_rope, const void* kv_latent, const void* k_rope,
                         const int32_t* page_table, const int32_t* seq_lens,
@@ -255,6 +270,7 @@ int snapmla_decode_bf16(const void* q_nope, const void* q_rope, const void* kv_l
                         float softmax_scale, int32_t causal,
                         int32_t num_splits, int32_t kv_chunk_tokens,
                         void* workspace, size_t workspace_bytes,
+                        void* out, int32_t out_dtype, float* lse,
                         hipStream_t stream);
 
 /*
@@ -273,7 +289,9 @@ int snapmla_append_bf16(const void* c_kv_new, const void* k_rope_new, const int3
  * kv_chunk_tokens and seq_lens as that call).  Per row:
  *     LSE = log sum_i exp(LSE_i),  o = sum_i exp(LSE_i - LSE) o_i
  * over the row's non-empty pieces.  A row that sees no token gets o = 0 and
- * LSE = -inf; a sequence flagged by a data error gets NaN.
+ * LSE = -inf; a sequence flagged by a data error gets NaN.  When the decode was
+ * given out, the rows it wrote (sequences that at most one piece covers) are
+ * left untouched: pass it the same out, out_dtype and lse.
  *
  *   out        [B][q_len][H][512], bf16 (out_dtype 0, round to nearest even) or float32 (1)
  *   lse        float32 [B][q_len][H], natural log of the sum of exp(s) (may be NULL)

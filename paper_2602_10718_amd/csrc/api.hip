@@ -72,12 +72,14 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
                   const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
                   int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
                   float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
-                  void* workspace, size_t workspace_bytes, hipStream_t stream, bool bf16_cache,
-                  const AppendIn& app = AppendIn(), int32_t flags = 0) {
+                  void* workspace, size_t workspace_bytes, void* out, int32_t out_dtype, float* lse,
+                  hipStream_t stream, bool bf16_cache, const AppendIn& app = AppendIn(), int32_t flags = 0) {
   int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
   if (st != SNAPMLA_OK) return st;
   if ((flags & ~SNAPMLA_DECODE_EXACT_QK) != 0)
     return fail(SNAPMLA_INVALID_ARGUMENT, "unknown decode flags 0x%x", (unsigned)flags);
+  if (out_dtype != 0 && out_dtype != 1) return fail(SNAPMLA_INVALID_ARGUMENT, "out_dtype must be 0 or 1");
+  if (!out && lse) return fail(SNAPMLA_INVALID_ARGUMENT, "lse without out: pass both or neither");
   if (page_size != 64) return fail(SNAPMLA_UNSUPPORTED, "page_size must be 64 (got %d)", page_size);
   if (max_pages < 1 || num_pages < 1)
     return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages and num_pages must be >= 1 (got %d, %d)", max_pages, num_pages);
@@ -87,11 +89,18 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   if ((int64_t)max_pages * 64 > 0x7FFFFFFF) return fail(SNAPMLA_INVALID_ARGUMENT, "max_pages too large");
   const snapmla::WsLayout L = snapmla::ws_layout(B, q_len, H, num_splits, kv_chunk_tokens);
   if (B == 0) return ok();
+  // Direct rows (out/lse written by the decode for sequences that one piece covers): the
+  // FP8-cache kernel writes them with one row group (R <= 64); with several it writes
+  // partials only and the combine writes every row.  The BF16-cache kernel writes them
+  // for any R.
+  void* dout = (bf16_cache || L.G == 1) ? out : nullptr;
+  float* dlse = dout ? lse : nullptr;
   if (!q_nope || !q_rope || !kv_latent || (!bf16_cache && !kv_scale) || !k_rope || !page_table || !seq_lens ||
       !workspace)
     return fail(SNAPMLA_INVALID_ARGUMENT, "null pointer argument");
   if (misaligned(q_nope) || misaligned(q_rope) || misaligned(kv_latent) || (!bf16_cache && misaligned(kv_scale)) ||
-      misaligned(k_rope) || misaligned4(page_table) || misaligned4(seq_lens) || misaligned(workspace))
+      misaligned(k_rope) || misaligned4(page_table) || misaligned4(seq_lens) || misaligned(workspace) ||
+      (out && misaligned(out)) || (lse && misaligned4(lse)))
     return fail(SNAPMLA_MISALIGNED, "pointer misaligned (int32/float32 index arrays need 4 bytes, data buffers 16)");
   if (workspace_bytes < L.total)
     return fail(SNAPMLA_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes (got %zu)", L.total, workspace_bytes);
@@ -108,7 +117,15 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   p.q_nope = static_cast<const uint16_t*>(q_nope);
   p.q8 = ws + L.q8;
   p.sq = reinterpret_cast<float*>(ws + L.sq);
-  p.rows = bf16_cache ? 0 : (int64_t)B * L.R;        // the BF16 cache reads the bf16 queries as they are
+  // row waves: query quantization (FP8 cache; the BF16 cache reads the bf16 queries as
+  // they are) and the rows of sequences without blocks (when out is given)
+  p.rows = (!bf16_cache || dout) ? (int64_t)B * L.R : 0;
+  p.quantize = !bf16_cache;
+  p.ctrl = reinterpret_cast<int32_t*>(ws + L.ctrl);
+  p.out = dout;
+  p.out_lse = dlse;
+  p.out_dtype = out_dtype;
+  p.R = L.R;
   p.seq_lens = seq_lens;
   p.prefix = reinterpret_cast<int32_t*>(ws + L.prefix);
   p.flags = reinterpret_cast<int32_t*>(ws + L.flags);
@@ -163,6 +180,9 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   d.sl2 = softmax_scale * 1.4426950408889634f;
   d.spin_limit = snapmla::spin_limit();
   d.qk_exact = (flags & SNAPMLA_DECODE_EXACT_QK) != 0 ? 1 : 0;
+  d.out = dout;
+  d.out_lse = dlse;
+  d.out_dtype = out_dtype;
   if (bf16_cache)
     return hip_status(snapmla::launch_decode_bf16(d, static_cast<const uint16_t*>(kv_latent), stream),
                       "decode_bf16 launch");
@@ -188,6 +208,7 @@ WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens)
   L.prefix = off; off += align256(((size_t)B + 1) * 4);
   L.flags = off;  off += align256((size_t)B * 4);
   L.zero = off;   off += 1024;
+  L.ctrl = off;   off += 256;
   L.units = kv_chunk_tokens == 0 ? num_splits : B * num_splits;   // <= 2^26 (check_shapes)
   L.desc = off;   off += align256((size_t)L.units * kDescInts * 4);
   L.lse = off;    off += align256((size_t)L.pieces * L.rows_pad * 4);
@@ -271,10 +292,11 @@ int snapmla_decode(const void* q_nope, const void* q_rope, const uint8_t* kv_lat
                    const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
                    int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
                    float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
-                   int32_t flags, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                   int32_t flags, void* workspace, size_t workspace_bytes, void* out, int32_t out_dtype, float* lse,
+                   hipStream_t stream) {
   return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
                        num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
-                       workspace_bytes, stream, false, AppendIn(), flags);
+                       workspace_bytes, out, out_dtype, lse, stream, false, AppendIn(), flags);
 }
 
 int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t n_new, const void* q_nope,
@@ -282,7 +304,8 @@ int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t 
                           const int32_t* page_table, const int32_t* seq_lens, int32_t B, int32_t q_len, int32_t H,
                           int32_t max_pages, int32_t num_pages, int32_t page_size, float softmax_scale,
                           int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens, int32_t flags,
-                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                          void* workspace, size_t workspace_bytes, void* out, int32_t out_dtype, float* lse,
+                          hipStream_t stream) {
   if (n_new < 0) return fail(SNAPMLA_INVALID_ARGUMENT, "n_new must be >= 0 (got %d)", n_new);
   AppendIn app;
   app.c_kv_new = c_kv_new;
@@ -290,17 +313,17 @@ int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t 
   app.n_new = n_new;
   return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
                        num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
-                       workspace_bytes, stream, false, app, flags);
+                       workspace_bytes, out, out_dtype, lse, stream, false, app, flags);
 }
 
 int snapmla_decode_bf16(const void* q_nope, const void* q_rope, const void* kv_latent, const void* k_rope,
                         const int32_t* page_table, const int32_t* seq_lens, int32_t B, int32_t q_len, int32_t H,
                         int32_t max_pages, int32_t num_pages, int32_t page_size, float softmax_scale,
                         int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens, void* workspace,
-                        size_t workspace_bytes, hipStream_t stream) {
+                        size_t workspace_bytes, void* out, int32_t out_dtype, float* lse, hipStream_t stream) {
   return decode_common(q_nope, q_rope, kv_latent, nullptr, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
                        num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
-                       workspace_bytes, stream, true);
+                       workspace_bytes, out, out_dtype, lse, stream, true);
 }
 
 int snapmla_append_bf16(const void* c_kv_new, const void* k_rope_new, const int32_t* page_table,
@@ -342,6 +365,7 @@ int snapmla_combine(const void* workspace, size_t workspace_bytes, const int32_t
   c.part_lse = reinterpret_cast<const float*>(ws + L.lse);
   c.prefix = reinterpret_cast<const int32_t*>(ws + L.prefix);
   c.flags = reinterpret_cast<const int32_t*>(ws + L.flags);
+  c.ctrl = reinterpret_cast<const int32_t*>(ws + L.ctrl);
   c.seq_lens = seq_lens;
   c.out = out;
   c.lse = lse;
@@ -505,7 +529,8 @@ int snapmla_append_decode_noalloc(const void* c_kv_new, const void* k_rope_new, 
   if (st != SNAPMLA_OK) return st;
   st = snapmla_append_decode(c_kv_new, k_rope_new, n_new, q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table,
                              seq_lens, B, q_len, H, max_pages, num_pages, page_size, softmax_scale, causal,
-                             num_splits, kv_chunk_tokens, flags, ws, SNAPMLA_NOALLOC_SCRATCH_BYTES, stream);
+                             num_splits, kv_chunk_tokens, flags, ws, SNAPMLA_NOALLOC_SCRATCH_BYTES, out, out_dtype,
+                             lse, stream);
   if (st != SNAPMLA_OK) return st;
   return snapmla_combine(ws, SNAPMLA_NOALLOC_SCRATCH_BYTES, seq_lens, B, q_len, H, num_splits, kv_chunk_tokens, out,
                          out_dtype, lse, stream);

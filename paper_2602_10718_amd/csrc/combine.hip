@@ -5,17 +5,14 @@
 //   LSE = log sum_p exp(LSE_p),   o = sum_p exp(LSE_p - LSE) * o_p.
 // One wave merges one row; lane l owns output dimensions 8l..8l+7.  The pieces'
 // log-sum-exps are read lane-parallel and the partial rows four at a time.
+// When the decode was given the output (ctrl[0] == 1) it has written the rows of
+// every sequence that at most one piece covers; those are left as they are.
 
+#include "piece_end.h"
 #include "snapmla_device.h"
 #include "snapmla_internal.h"
 
 namespace snapmla {
-
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
-  const uint32_t u = __float_as_uint(x);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
 
 __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   const int lane = threadIdx.x & 63;
@@ -41,6 +38,9 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
       last = (nb + a.chunk_blocks - 1) / a.chunk_blocks - 1;
     }
   }
+  // (a sequence with blocks meets only non-empty parts, so last - first + 1 is its
+  // piece count)
+  if (a.ctrl[0] == 1 && last <= first) return;
   auto exists = [&](int i) -> bool {
     if (!balanced) return true;
     return (int64_t)i * T / W < (int64_t)(i + 1) * T / W;
@@ -120,10 +120,10 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
     dst[1] = v4f{o[4], o[5], o[6], o[7]};
   } else {
     uint4 pk;
-    pk.x = f32_to_bf16_rne(o[0]) | (f32_to_bf16_rne(o[1]) << 16);
-    pk.y = f32_to_bf16_rne(o[2]) | (f32_to_bf16_rne(o[3]) << 16);
-    pk.z = f32_to_bf16_rne(o[4]) | (f32_to_bf16_rne(o[5]) << 16);
-    pk.w = f32_to_bf16_rne(o[6]) | (f32_to_bf16_rne(o[7]) << 16);
+    pk.x = f32_to_bf16_bits(o[0]) | (f32_to_bf16_bits(o[1]) << 16);
+    pk.y = f32_to_bf16_bits(o[2]) | (f32_to_bf16_bits(o[3]) << 16);
+    pk.z = f32_to_bf16_bits(o[4]) | (f32_to_bf16_bits(o[5]) << 16);
+    pk.w = f32_to_bf16_bits(o[6]) | (f32_to_bf16_bits(o[7]) << 16);
     reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.out) + orow * kDc)[lane] = pk;
   }
   if (a.lse != nullptr && lane == 0) a.lse[orow] = lse;

@@ -64,6 +64,7 @@
 // stale bytes; their logits are masked to -inf, their fused probabilities
 // forced to 0 and their V bytes cleared before the PV product.
 
+#include "piece_end.h"
 #include "snapmla_device.h"
 #include "snapmla_internal.h"
 
@@ -88,9 +89,6 @@ constexpr int kXpBase = kXBase + kXcBytes + kXgBytes + kXfBytes;
 constexpr int kSmemBytes = kXpBase + kXpBytes;
 static_assert(kSmemBytes <= 160 * 1024, "LDS budget of one workgroup");
 constexpr float kLn2 = 0.69314718055994531f;
-// store instructions of one PV wave at the end of a piece: 2 row tiles x
-// (16 output chunks + 1 log-sum-exp)
-constexpr int kPieceStores = 2 * (16 + 1);
 static_assert(20 + kPieceStores < 64, "wait counter range");
 
 // Branch weights for the block layout: the rare cases of a period (a piece start
@@ -107,6 +105,24 @@ static_assert(20 + kPieceStores < 64, "wait counter range");
 // t0+16..t0+19) to eight distinct groups of a 128-byte line.
 __device__ __forceinline__ int swz(int t) { return (t & 15) ^ (((t >> 4) & 1) << 2); }
 __device__ __forceinline__ int rswz(int t) { return (t >> 1) & 7; }
+
+// Per-row results at a piece end from the published state {gamma, l, m, sigma_P} of
+// the row's last block: 1/l and LSE = ln 2 (m + log2(sigma_P l)) (m in log2 units;
+// Algorithm 1 finalisation); 0 and -inf for a row without tokens, NaN for a bad piece.
+__device__ __forceinline__ void piece_row_results(v4f gl0, v4f gl1, bool bad, float (&inv)[2], float (&lse)[2]) {
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const v4f gl = r == 0 ? gl0 : gl1;
+    const float lfin = gl[1];
+    const bool empty = !(lfin > 0.0f);
+    inv[r] = empty ? 0.0f : 1.0f / lfin;
+    lse[r] = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
+    if (bad) {
+      inv[r] = __builtin_nanf("");
+      lse[r] = __builtin_nanf("");
+    }
+  }
+}
 
 // Handshake flags in LDS.  A wave's LDS operations complete in issue order, so
 // a flag stored after lds_wait_all() is seen only after the data stored before it.
@@ -568,39 +584,14 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           // ---- end of a piece: write the normalized partial output and LSE ----
           // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
           if (unlikely(k == nblocks || gstart + k >= cur_end)) {
+            // the piece of block k-1 ends: exactly kPieceStores stores (the next
+            // top-of-period wait counts them); every wave writes the same LSEs
             const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
                                                     : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
-            const float nanv = __builtin_nanf("");
-            // Exactly kPieceStores store instructions per wave, whatever R: rows up to
-            // rows_pad lie inside the piece's slot (the combine reads rows < R only),
-            // and every wave writes the same LSE values.  The next top-of-period wait
-            // counts them.
-  #pragma unroll
-            for (int r = 0; r < 2; ++r) {
-              const int row = r == 0 ? row0 : row1;
-              const v4f gl = r == 0 ? gl0 : gl1;
-              const float lfin = gl[1];
-              const bool empty = !(lfin > 0.0f);
-              float inv = empty ? 0.0f : 1.0f / lfin;
-              if (cur_bad) inv = nanv;
-              float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
-  #pragma unroll
-              for (int T = 0; T < 4; ++T) {
-  #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                  *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
-                      v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
-                          O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
-                  __builtin_amdgcn_sched_barrier(0);
-                }
-              }
-              if (h == 0) {
-                float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
-                if (cur_bad) lse = nanv;
-                a.part_lse[pid * a.rows_pad + row] = lse;
-              }
-              __builtin_amdgcn_sched_barrier(0);
-            }
+            const bool whole = cur_blk0 == 0 && gstart + k >= cur_end;   // the piece is its whole sequence
+            float inv[2], lse[2];
+            piece_row_results(gl0, gl1, cur_bad, inv, lse);
+            store_piece(a, O, inv[0], inv[1], lse[0], lse[1], row0, row1, dq, h, pid, cur_b, whole);
   #pragma unroll
             for (int T = 0; T < 8; ++T) O[T] = v16f{0};
             stored = true;
@@ -716,6 +707,7 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
                                                 : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
         const bool close_bad = cur_bad;
+        const int close_b = cur_b;
         if (RD) {
           // ---- block k: piece bookkeeping (mirrors the QK waves) ---------------
           const int gb = gstart + k;
@@ -773,37 +765,12 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           // ---- end of a piece: write the normalized partial output and LSE --
           // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
           if (unlikely(close)) {
-            const float nanv = __builtin_nanf("");
-            // Exactly kPieceStores store instructions per wave, whatever R: rows up to
-            // rows_pad lie inside the piece's slot (the combine reads rows < R only),
-            // and every wave writes the same LSE values.  The next top-of-period
-            // waits count them.
-  #pragma unroll
-            for (int r = 0; r < 2; ++r) {
-              const int row = r == 0 ? row0 : row1;
-              const v4f gl = r == 0 ? gl0 : gl1;
-              const float lfin = gl[1];
-              const bool empty = !(lfin > 0.0f);
-              float inv = empty ? 0.0f : 1.0f / lfin;
-              if (close_bad) inv = nanv;
-              float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
-  #pragma unroll
-              for (int T = 0; T < 4; ++T) {
-  #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                  *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
-                      v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
-                          O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
-                  __builtin_amdgcn_sched_barrier(0);
-                }
-              }
-              if (h == 0) {
-                float lse = empty ? -INFINITY : (gl[2] + log2f(gl[3] * lfin)) * kLn2;
-                if (close_bad) lse = nanv;
-                a.part_lse[pid * a.rows_pad + row] = lse;
-              }
-              __builtin_amdgcn_sched_barrier(0);
-            }
+            // exactly kPieceStores stores (the next top-of-period waits count them)
+            float inv[2], lse[2];
+            piece_row_results(gl0, gl1, close_bad, inv, lse);
+            // (partials only with several row groups: the direct-row stores would raise this
+            // schedule's register pressure into spills; the launch leaves out unset)
+            store_piece(a, O, inv[0], inv[1], lse[0], lse[1], row0, row1, dq, h, pid, close_b, false);
   #pragma unroll
             for (int T = 0; T < 8; ++T) O[T] = v16f{0};
             st1 = true;

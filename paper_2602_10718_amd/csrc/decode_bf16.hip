@@ -19,6 +19,7 @@
 // (ds_read_b64_tr_b16: in each 16-lane group, lane 4q + c receives element c of
 // the 8-byte pieces addressed by lanes q, q+4, q+8, q+12).
 
+#include "piece_end.h"
 #include "snapmla_device.h"
 #include "snapmla_internal.h"
 
@@ -41,7 +42,7 @@ constexpr int kFBase = kGBase + kGBytes;                // QK flags
 constexpr int kRingBase = kFBase + 16;                  // page-id ring [PV wave][4]
 constexpr int kSmem = kRingBase + 64;
 static_assert(kSmem <= 160 * 1024, "LDS budget of one workgroup");
-constexpr int kStores = 2 * (16 + 1);                   // piece-end stores of a PV wave
+constexpr int kStores = kPieceStores;                    // piece-end stores of a PV wave
 static_assert(18 + kStores < 64, "wait counter range");
 constexpr float kLn2f = 0.69314718055994531f;
 
@@ -334,35 +335,24 @@ __global__ __launch_bounds__(512, 1) void decode_bf16_kernel(DecodeArgs a, const
           }
         }
         if (k == nblk || ((k & 1) == 0 && gstart + (k >> 1) >= cur_end)) {
+          // the piece ends: exactly kStores stores (the next top-of-period wait counts them)
           const int64_t pid = a.chunk_blocks == 0 ? (int64_t)unit + cur_b
                                                   : (int64_t)cur_b * a.num_splits + cur_blk0 / a.chunk_blocks;
-          const float nanv = __builtin_nanf("");
+          const bool whole = cur_blk0 == 0 && gstart + (k >> 1) >= cur_end;   // the piece is its whole sequence
+          float inv[2], lse[2];
 #pragma unroll
           for (int r = 0; r < 2; ++r) {
-            const int row = r == 0 ? row0 : row1;
             const v4f gl = r == 0 ? gl0 : gl1;
             const float lfin = gl[1];
             const bool empty = !(lfin > 0.0f);
-            float inv = empty ? 0.0f : 1.0f / lfin;
-            if (cur_bad) inv = nanv;
-            float* po = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
-#pragma unroll
-            for (int T = 0; T < 4; ++T) {
-#pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                *reinterpret_cast<v4f*>(po + 32 * T + 8 * q) =
-                    v4f{O[2 * T + r][4 * q + 0] * inv, O[2 * T + r][4 * q + 1] * inv,
-                        O[2 * T + r][4 * q + 2] * inv, O[2 * T + r][4 * q + 3] * inv};
-                __builtin_amdgcn_sched_barrier(0);
-              }
+            inv[r] = empty ? 0.0f : 1.0f / lfin;
+            lse[r] = empty ? -INFINITY : (gl[2] + log2f(lfin)) * kLn2f;
+            if (cur_bad) {
+              inv[r] = __builtin_nanf("");
+              lse[r] = __builtin_nanf("");
             }
-            if (h == 0) {
-              float lse = empty ? -INFINITY : (gl[2] + log2f(lfin)) * kLn2f;
-              if (cur_bad) lse = nanv;
-              a.part_lse[pid * a.rows_pad + row] = lse;
-            }
-            __builtin_amdgcn_sched_barrier(0);
           }
+          store_piece(a, O, inv[0], inv[1], lse[0], lse[1], row0, row1, dq, h, pid, cur_b, whole);
 #pragma unroll
           for (int T = 0; T < 8; ++T) O[T] = v16f{0};
           stored = true;

@@ -107,9 +107,8 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
     for (int b = b0; b < b1; ++b) {
       const int n = a.seq_lens[b];
       if (per == 1) lens[tid] = n;
-      bool ok = (n == 0) || (n >= a.q_len && n <= a.max_pages * kPage);
+      const bool ok = seq_len_ok(n, a.q_len, a.max_pages, a.chunk_blocks, a.num_splits);
       const int nb = (n + kPage - 1) / kPage;
-      if (ok && a.chunk_blocks > 0) ok = (nb + a.chunk_blocks - 1) / a.chunk_blocks <= a.num_splits;
       a.flags[b] = ok ? 0 : 1;
       local += ok ? nb : 0;
     }
@@ -129,6 +128,7 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
       a.prefix[b + 1] = run;
     }
     reinterpret_cast<uint32_t*>(a.zero)[tid] = 0u;   // 256 threads x 4 B = 1 KiB
+    if (tid == 0) a.ctrl[0] = a.out != nullptr ? 1 : 0;
     __syncthreads();                                 // prefix complete (LDS and global)
 
     // ---- start descriptors, one unit per thread ----------------------------
@@ -176,10 +176,31 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
                         a.kv_latent, a.kv_scale, a.k_rope, lane);
     return;
   }
-  const int q0 = 1 + a.ablocks;                    // first query-quantization workgroup
+  const int q0 = 1 + a.ablocks;                    // first row workgroup
   const int64_t nw = (int64_t)(gridDim.x - q0) * 4;
-  for (int64_t r = (int64_t)(blockIdx.x - q0) * 4 + (tid >> 6); r < a.rows; r += nw)
-    quantize_row_wave(a.q_nope + r * kDc, a.q8 + r * kDc, a.sq + r, lane);
+  for (int64_t r = (int64_t)(blockIdx.x - q0) * 4 + (tid >> 6); r < a.rows; r += nw) {
+    // (the length is loaded first so that its round trip overlaps the quantization's)
+    const int n = a.out != nullptr ? a.seq_lens[r / a.R] : 0;
+    if (a.quantize) quantize_row_wave(a.q_nope + r * kDc, a.q8 + r * kDc, a.sq + r, lane);
+    if (a.out != nullptr) {
+      // a row of a sequence without blocks is final here: 0 and -inf for an empty
+      // sequence, NaN for one a data error rejects (the decode writes no piece for it)
+      const bool ok = seq_len_ok(n, a.q_len, a.max_pages, a.chunk_blocks, a.num_splits);
+      if (!ok || n == 0) {
+        const float v = ok ? 0.0f : __builtin_nanf("");
+        if (a.out_dtype == 1) {
+          v4f* dst = reinterpret_cast<v4f*>(static_cast<float*>(a.out) + r * kDc) + 2 * lane;
+          dst[0] = v4f{v, v, v, v};
+          dst[1] = v4f{v, v, v, v};
+        } else {
+          const int bv = ok ? 0 : 0x7FC0;
+          reinterpret_cast<v4i*>(static_cast<uint16_t*>(a.out) + r * kDc)[lane] =
+              v4i{bv | (bv << 16), bv | (bv << 16), bv | (bv << 16), bv | (bv << 16)};
+        }
+        if (a.out_lse != nullptr && lane == 0) a.out_lse[r] = ok ? -INFINITY : __builtin_nanf("");
+      }
+    }
+  }
 }
 
 static int grid_for(int64_t waves) {

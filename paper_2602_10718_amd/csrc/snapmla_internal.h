@@ -11,7 +11,7 @@ namespace snapmla {
 struct WsLayout {
   int R = 0, G = 0, rows_pad = 0, pieces = 0;
   int units = 0;
-  size_t q8 = 0, sq = 0, prefix = 0, flags = 0, zero = 0, desc = 0, lse = 0, o = 0, total = 0;
+  size_t q8 = 0, sq = 0, prefix = 0, flags = 0, zero = 0, ctrl = 0, desc = 0, lse = 0, o = 0, total = 0;
 };
 WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens);
 
@@ -26,6 +26,16 @@ struct PrepArgs {
   uint8_t* zero;            // 1 KiB that the decode kernel reads in place of slots past a sequence end
   int32_t* desc;            // [units][kDescInts] start descriptor of each split unit (see kDesc*)
   int B, q_len, max_pages, chunk_blocks, num_splits, units;
+  // Final results written by the decode itself (out != nullptr): the rows of sequences
+  // without blocks (empty: o = 0, LSE = -inf; rejected by a data error: NaN), written by
+  // the row waves, and ctrl[0] = 1, which tells the combine that the decode also wrote
+  // every sequence one piece covers (ctrl[0] = 0 when out is null: partials only).
+  int32_t* ctrl = nullptr;
+  void* out = nullptr;              // [B*R][512] bf16 (out_dtype 0) or f32 (1)
+  float* out_lse = nullptr;         // [B*R] or null
+  int out_dtype = 0, R = 0;
+  bool quantize = true;             // the row waves quantize the queries (FP8 cache) or only
+                                    // write the rows of sequences without blocks
   // optional fused quantize-on-append of n_new tokens per sequence (ablocks workgroups of
   // four tokens; none when ablocks == 0), run beside the query quantization
   const uint16_t* c_kv_new = nullptr;   // [B][n_new][512]
@@ -77,13 +87,28 @@ struct DecodeArgs {
   // QK content product with exact float32 accumulation (F16 MFMA on the exactly
   // converted E4M3 codes) instead of the FP8 MFMA
   int qk_exact = 0;
+  // Direct results (out != nullptr): a piece that covers its whole sequence writes the
+  // final rows and LSEs there instead of a partial (the one-piece merge is exact).
+  void* out = nullptr;              // [B*R][512] bf16 (out_dtype 0) or f32 (1)
+  float* out_lse = nullptr;         // [B*R] or null
+  int out_dtype = 0;
 };
+
+// Validity of a sequence's length (the data errors of the decode): true when the
+// length is usable, i.e. 0, or q_len .. max_pages*64 tokens (and, with fixed chunks,
+// at most num_splits chunks).  Shared by the plan and the rows of rejected sequences.
+__host__ __device__ inline bool seq_len_ok(int n, int q_len, int max_pages, int chunk_blocks, int num_splits) {
+  bool ok = (n == 0) || (n >= q_len && (int64_t)n <= (int64_t)max_pages * 64);
+  if (ok && chunk_blocks > 0) ok = ((n + 63) / 64 + chunk_blocks - 1) / chunk_blocks <= num_splits;
+  return ok;
+}
 
 struct CombineArgs {
   const float* part_o;
   const float* part_lse;
   const int32_t* prefix;
   const int32_t* flags;
+  const int32_t* ctrl;      // ctrl[0] == 1: sequences with at most one piece are final already
   const int32_t* seq_lens;
   void* out;
   float* lse;

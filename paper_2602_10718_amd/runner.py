@@ -33,15 +33,21 @@ class DecodeRunner:
     """
 
     def __init__(self, wl, num_splits=None, kv_chunk_tokens=None, out_dtype=torch.float32, fill=True, cache=None,
-                 kv_dtype="e4m3", exact_qk=False):
+                 kv_dtype="e4m3", exact_qk=False, direct=True, unsplit=False):
         """cache: (kv_latent, kv_scale, k_rope) of another runner over the same sequences, pages and
         tokens, used instead of allocating and filling a new one.  kv_dtype "bf16": a BF16 cache
         (kv_latent bf16, no scales) written by snapmla_append_bf16 and read by snapmla_decode_bf16.
-        exact_qk: decode with SNAPMLA_DECODE_EXACT_QK (content term accumulated exactly in float32)."""
+        exact_qk: decode with SNAPMLA_DECODE_EXACT_QK (content term accumulated exactly in float32).
+        direct: the decode writes the rows of sequences that one piece covers into out/lse itself
+        (False: partials only, every row from the combine).  unsplit: one piece per sequence (fixed
+        chunks as long as the page table, one split), so that the step needs no combine."""
         self.kv_dtype = kv_dtype
         self.flags = sm.DECODE_EXACT_QK if exact_qk else 0
         self.wl = wl
         self.B, self.H, self.q_len = wl.B, wl.H, wl.q_len
+        self.direct = direct
+        if unsplit:
+            kv_chunk_tokens, num_splits = wl.max_pages * PAGE, 1
         self.kv_chunk_tokens = wl.kv_chunk_tokens if kv_chunk_tokens is None else kv_chunk_tokens
         if num_splits is None:
             if self.kv_chunk_tokens > 0:
@@ -50,6 +56,11 @@ class DecodeRunner:
                 num_splits = sm.default_num_splits(self.q_len, self.H,
                                                    total_blocks=int(((wl.seq_lens.astype(np.int64) + 63) // 64).sum()))
         self.num_splits = num_splits
+        # with fixed chunks as long as the page table and one split, no sequence is split: the decode
+        # writes every row (direct) and the combine has nothing to do
+        # (the FP8-cache decode writes direct rows with one 64-row group; the BF16-cache decode always)
+        direct_rows = direct and (kv_dtype == "bf16" or self.q_len * self.H <= 64)
+        self.needs_combine = not (direct_rows and self.kv_chunk_tokens >= wl.max_pages * PAGE and num_splits == 1)
         P = wl.num_pages
         if cache is not None:
             self.kv_latent, self.kv_scale, self.k_rope = cache
@@ -111,15 +122,19 @@ class DecodeRunner:
         sm.snapmla_quantize_append(self.new_ckv, self.new_krope, self.page_table, self.seq_lens, self.wl.num_pages,
                                    self.kv_latent, self.kv_scale, self.k_rope, stream=stream)
 
+    def _out(self):
+        return (self.out, self.lse) if self.direct else (None, None)
+
     def decode(self, stream=None):
+        out, lse = self._out()
         if self.kv_dtype == "bf16":
             sm.snapmla_decode_bf16(self.q_nope, self.q_rope, self.kv_latent, self.k_rope, self.page_table,
                                    self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits,
-                                   self.kv_chunk_tokens, self.workspace, stream=stream)
+                                   self.kv_chunk_tokens, self.workspace, stream=stream, out=out, lse=lse)
             return
         sm.snapmla_decode(self.q_nope, self.q_rope, self.kv_latent, self.kv_scale, self.k_rope, self.page_table,
                           self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits, self.kv_chunk_tokens,
-                          self.workspace, stream=stream, flags=self.flags)
+                          self.workspace, stream=stream, flags=self.flags, out=out, lse=lse)
 
     def combine(self, stream=None):
         sm.snapmla_combine(self.workspace, self.seq_lens, self.B, self.q_len, self.H, self.num_splits,
@@ -127,10 +142,11 @@ class DecodeRunner:
 
     def append_decode(self, stream=None):
         """The step's append and decode in one call (the append runs in the decode's preparation launch)."""
+        out, lse = self._out()
         sm.snapmla_append_decode(self.new_ckv, self.new_krope, self.q_nope, self.q_rope, self.kv_latent, self.kv_scale,
                                  self.k_rope, self.page_table, self.seq_lens, self.wl.tau, self.wl.causal,
                                  self.num_splits, self.kv_chunk_tokens, self.workspace, stream=stream,
-                                 flags=self.flags)
+                                 flags=self.flags, out=out, lse=lse)
 
     def step(self, stream=None):
         if self.kv_dtype == "bf16":
@@ -138,7 +154,8 @@ class DecodeRunner:
             self.decode(stream)
         else:
             self.append_decode(stream)
-        self.combine(stream)
+        if self.needs_combine:
+            self.combine(stream)
 
     def sequence_cache(self, b):
         """(codes uint8 [N, 512], scales f32 [N], rope bits uint16 [N, 64]) of sequence b read back via the page table;

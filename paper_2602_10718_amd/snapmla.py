@@ -43,7 +43,7 @@ lib.snapmla_decode_workspace_size.restype = ctypes.c_int
 lib.snapmla_decode_workspace_size.argtypes = [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
 lib.snapmla_decode.restype = ctypes.c_int
 lib.snapmla_decode.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
-                               _i32, _i32, _p, _sz, _p]
+                               _i32, _i32, _p, _sz, _p, _i32, _p, _p]
 lib.snapmla_combine.restype = ctypes.c_int
 lib.snapmla_combine.argtypes = [_p, _sz, _p, _i32, _i32, _i32, _i32, _i32, _p, _i32, _p, _p]
 lib.snapmla_e4m3_encode.restype = ctypes.c_int
@@ -52,14 +52,14 @@ lib.snapmla_quantize_cache_config.restype = ctypes.c_int
 lib.snapmla_quantize_cache_config.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p]
 lib.snapmla_decode_bf16.restype = ctypes.c_int
 lib.snapmla_decode_bf16.argtypes = [_p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
-                                    _i32, _p, _sz, _p]
+                                    _i32, _p, _sz, _p, _i32, _p, _p]
 lib.snapmla_append_bf16.restype = ctypes.c_int
 lib.snapmla_append_bf16.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p]
 lib.snapmla_fetch_dequant.restype = ctypes.c_int
 lib.snapmla_fetch_dequant.argtypes = [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]
 lib.snapmla_append_decode.restype = ctypes.c_int
 lib.snapmla_append_decode.argtypes = [_p, _p, _i32, _p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32,
-                                      _f32, _i32, _i32, _i32, _i32, _p, _sz, _p]
+                                      _f32, _i32, _i32, _i32, _i32, _p, _sz, _p, _i32, _p, _p]
 lib.snapmla_debug_read_ceiling.restype = ctypes.c_int
 lib.snapmla_debug_mfma_fp8.restype = ctypes.c_int
 lib.snapmla_debug_mfma_fp8.argtypes = [_p, _p, _p, _i64, _p]
@@ -159,29 +159,42 @@ def snapmla_decode_workspace_size(B, q_len, H, num_splits, kv_chunk_tokens):
 DECODE_EXACT_QK = 1   # snapmla_decode_flags: content term with exact float32 accumulation
 
 
+def _out_args(out, lse):
+    """(out pointer, out_dtype, lse pointer) of the decode calls; out None: partials only."""
+    if out is None:
+        if lse is not None:
+            raise ValueError("lse without out")
+        return None, 0, None
+    return _ptr(out), _out_dtype(out), _ptr(lse)
+
+
 def snapmla_decode(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, softmax_scale, causal,
-                   num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None, flags=0):
+                   num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None, flags=0, out=None, lse=None):
     """q_nope bf16 [B, q_len, H, 512], q_rope bf16 [B, q_len, H, 64]; cache planes as in snapmla_quantize_append;
-    workspace uint8 of at least snapmla_decode_workspace_size(...) bytes; flags 0 or DECODE_EXACT_QK."""
+    workspace uint8 of at least snapmla_decode_workspace_size(...) bytes; flags 0 or DECODE_EXACT_QK.
+    out bf16 or f32 [B, q_len, H, 512] and lse f32 [B, q_len, H] (or None): the rows of sequences that one
+    piece covers are written here directly, the others by snapmla_combine with the same out/lse."""
     B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
     _check(lib.snapmla_decode(_ptr(q_nope), _ptr(q_rope), _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope),
                               _ptr(page_table), _ptr(seq_lens), B, q_len, H, page_table.shape[1], kv_latent.shape[0],
                               page_size, float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, int(flags),
-                              _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+                              _ptr(workspace), workspace.numel() * workspace.element_size(), *_out_args(out, lse),
+                              _stream(stream)))
 
 
 def snapmla_append_decode(c_kv_new, k_rope_new, q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens,
                           softmax_scale, causal, num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None,
-                          flags=0):
+                          flags=0, out=None, lse=None):
     """snapmla_quantize_append of c_kv_new bf16 [B, n_new, 512] / k_rope_new bf16 [B, n_new, 64] followed by
-    snapmla_decode, the append run in the decode's preparation launch."""
+    snapmla_decode (out, lse as there), the append run in the decode's preparation launch."""
     B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
     n_new = c_kv_new.shape[1]
     _check(lib.snapmla_append_decode(_ptr(c_kv_new), _ptr(k_rope_new), n_new, _ptr(q_nope), _ptr(q_rope),
                                      _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope), _ptr(page_table), _ptr(seq_lens),
                                      B, q_len, H, page_table.shape[1], kv_latent.shape[0], page_size,
                                      float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, int(flags),
-                                     _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     *_out_args(out, lse), _stream(stream)))
 
 
 NOALLOC_SCRATCH_BYTES = 128 << 20   # SNAPMLA_NOALLOC_SCRATCH_BYTES
@@ -255,13 +268,14 @@ def snapmla_quantize_cache_config(c_kv, k_rope, page_table, cu_seqlens, config, 
 
 
 def snapmla_decode_bf16(q_nope, q_rope, kv_latent, k_rope, page_table, seq_lens, softmax_scale, causal, num_splits,
-                        kv_chunk_tokens, workspace, page_size=64, stream=None):
+                        kv_chunk_tokens, workspace, page_size=64, stream=None, out=None, lse=None):
     """kv_latent bf16 [num_pages, 64, 512]; otherwise as snapmla_decode (without kv_scale)."""
     B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
     _check(lib.snapmla_decode_bf16(_ptr(q_nope), _ptr(q_rope), _ptr(kv_latent), _ptr(k_rope), _ptr(page_table),
                                    _ptr(seq_lens), B, q_len, H, page_table.shape[1], kv_latent.shape[0], page_size,
                                    float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, _ptr(workspace),
-                                   workspace.numel() * workspace.element_size(), _stream(stream)))
+                                   workspace.numel() * workspace.element_size(), *_out_args(out, lse),
+                                   _stream(stream)))
 
 
 def snapmla_append_bf16(c_kv_new, k_rope_new, page_table, seq_lens, num_pages, kv_latent, k_rope, page_size=64,

@@ -36,7 +36,7 @@ def test_every_declared_symbol_is_exported(sm):
 
 
 def test_abi_version(sm):
-    assert sm.snapmla_abi_version() == 2
+    assert sm.snapmla_abi_version() == 3
 
 
 def test_spin_limit_hook_validates(sm):
@@ -69,32 +69,42 @@ def test_workspace_size_rejects(sm, args, status):
 def test_decode_argument_errors_before_any_launch(sm):
     L = sm.lib
     # unsupported page size
-    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, 0, None, 0, None)
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, 0, None, 0, None, 0, None, None)
     assert st == 2
     # bad softmax scale
-    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, float("nan"), 0, 8, 0, 0, None, 0,
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, float("nan"), 0, 8, 0, 0, None, 0, None, 0, None,
                           None)
     assert st == 1
     # null pointers
-    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, None, 0, None)
+    st = L.snapmla_decode(None, None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, None, 0, None, 0, None, None)
     assert st == 1 and "null" in sm.snapmla_get_last_error()
     # misaligned pointer (never dereferenced: validation fails first)
     p = 16 * 1024 + 8
-    st = L.snapmla_decode(p, p, p, p, p, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096, 1 << 30, None)
+    st = L.snapmla_decode(p, p, p, p, p, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096, 1 << 30, None, 0, None, None)
     assert st == 4
     # workspace too small
-    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096, 16, None)
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096, 16, None, 0, None, None)
     assert st == 3
     # causal flag
-    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 7, 8, 0, 0, 4096, 1 << 30,
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 7, 8, 0, 0, 4096, 1 << 30, None, 0, None,
                           None)
     assert st == 1
     # unknown decode flags
     st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 2, 4096,
-                          1 << 30, None)
+                          1 << 30, None, 0, None, None)
     assert st == 1 and "flags" in sm.snapmla_get_last_error()
+    # out_dtype out of range; lse without out; misaligned out
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096,
+                          1 << 30, 4096, 2, None, None)
+    assert st == 1 and "out_dtype" in sm.snapmla_get_last_error()
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096,
+                          1 << 30, None, 0, 4096, None)
+    assert st == 1 and "lse" in sm.snapmla_get_last_error()
+    st = L.snapmla_decode(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, 4096,
+                          1 << 30, 4104, 0, 4096, None)
+    assert st == 4
     # empty batch is a no-op
-    assert L.snapmla_decode(None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, None, 0,
+    assert L.snapmla_decode(None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0, None, 0, None, 0, None,
                             None) == 0
 
 
@@ -127,17 +137,17 @@ def test_fetch_dequant_validates(sm):
 def test_bf16_entry_points_validate(sm):
     L = sm.lib
     # decode_bf16: same checks as snapmla_decode, no scale plane
-    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, None, 0,
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 1, 16, 4, 8, 32, 0.1, 0, 8, 0, None, 0, None, 0, None,
                                  None) == 2                                                     # page size
-    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 3, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 3, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0, None, 0, None,
                                  None) == 1                                                     # q_len
-    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0, None, 0, None,
                                  None) == 1                                                     # null pointers
-    assert L.snapmla_decode_bf16(4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096, 16,
+    assert L.snapmla_decode_bf16(4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096, 16, None, 0, None,
                                  None) == 3                                                     # workspace
     assert L.snapmla_decode_bf16(4096, 4096, 4104, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 4096,
-                                 1 << 30, None) == 4                                            # misaligned cache
-    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0,
+                                 1 << 30, None, 0, None, None) == 4                                            # misaligned cache
+    assert L.snapmla_decode_bf16(None, None, None, None, None, None, 0, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, None, 0, None, 0, None,
                                  None) == 0                                                     # B == 0
     # append_bf16
     assert L.snapmla_append_bf16(None, None, None, None, 1, 1, 4, 4, 32, None, None, None) == 2
@@ -175,12 +185,12 @@ def test_append_decode_validates(sm):
     big = 1 << 30
     # n_new < 0; then the decode's own checks (q_len 3); then null / misaligned new-token pointers
     assert L.snapmla_append_decode(None, None, -1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 0, 4096, big, None) == 1
+                                   0.1, 0, 8, 0, 0, 4096, big, None, 0, None, None) == 1
     assert L.snapmla_append_decode(4096, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 3, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 0, 4096, big, None) == 1
+                                   0.1, 0, 8, 0, 0, 4096, big, None, 0, None, None) == 1
     assert L.snapmla_append_decode(None, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 0, 4096, big, None) == 1
+                                   0.1, 0, 8, 0, 0, 4096, big, None, 0, None, None) == 1
     assert L.snapmla_append_decode(4104, 4096, 1, 4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 0, 4096, big, None) == 4
+                                   0.1, 0, 8, 0, 0, 4096, big, None, 0, None, None) == 4
     assert L.snapmla_append_decode(None, None, 1, None, None, None, None, None, None, None, 0, 1, 16, 4, 8, 64,
-                                   0.1, 0, 8, 0, 0, None, 0, None) == 0                            # B == 0
+                                   0.1, 0, 8, 0, 0, None, 0, None, 0, None, None) == 0                            # B == 0
