@@ -4,7 +4,9 @@ One step = the whole hot path for one batch: quantize-and-append the step's new
 tokens into the paged FP8 cache (snapmla_quantize_append), quantize the queries
 and decode every sequence (snapmla_decode: FP8 QK + BF16 RoPE, online softmax,
 fused and block-quantized P, FP8 PV), and merge the split-KV pieces
-(snapmla_combine).  Inputs are resident in HBM before timing starts.
+(snapmla_combine; skipped under the unsplit plan, where the decode writes every
+row itself -- the plan bench.py picks for small batches, --plan).  Inputs are
+resident in HBM before timing starts.
 
 Default workload: 64-head MLA decode, batch 64, one query token, ragged context
 lengths uniform in [8192, 32768], 64-token pages in shuffled physical order.
@@ -557,7 +559,10 @@ def accuracy_vs_bf16(run, w, samples=8):
     from paper_2602_10718_amd import snapmla as sm
     out32 = torch.empty((w.B, w.q_len, w.H, 512), dtype=torch.float32, device="cuda")
     lse32 = torch.empty((w.B, w.q_len, w.H), dtype=torch.float32, device="cuda")
-    run.append_decode()
+    # (the decode writes the rows it finalises itself into the same float32 output)
+    sm.snapmla_append_decode(run.new_ckv, run.new_krope, run.q_nope, run.q_rope, run.kv_latent, run.kv_scale,
+                             run.k_rope, run.page_table, run.seq_lens, w.tau, w.causal, run.num_splits,
+                             run.kv_chunk_tokens, run.workspace, flags=run.flags, out=out32, lse=lse32)
     sm.snapmla_combine(run.workspace, run.seq_lens, w.B, w.q_len, w.H, run.num_splits, run.kv_chunk_tokens, out32,
                        lse32)
     torch.cuda.synchronize()
@@ -602,6 +607,9 @@ def main():
     ap.add_argument("--workload", default="headline",
                     choices=("tiny", "dsv3", "headline", "longsplit", "mtp"), help="workload by name")
     ap.add_argument("--num-splits", type=int, default=None)
+    ap.add_argument("--plan", default="auto", choices=["auto", "balanced", "unsplit"],
+                    help="split plan: balanced block ranges (+ combine), one piece per sequence (no combine), or "
+                         "auto: the unsplit plan where the runner expects it to be faster (small batches)")
     ap.add_argument("--cold-steps", type=int, default=50, help="cold-cache steps (0 to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--op", default="decode", choices=["decode", "fetch_dequant", "sweep", "ablation", "decode_bf16"],
@@ -633,7 +641,8 @@ def main():
         return
     w = wl.make(args.workload)
     t_fill = time.perf_counter()
-    run = DecodeRunner(w, num_splits=args.num_splits, out_dtype=torch.bfloat16)
+    run = DecodeRunner(w, num_splits=args.num_splits, out_dtype=torch.bfloat16,
+                       unsplit={"auto": "auto", "balanced": False, "unsplit": True}[args.plan])
     t_fill = time.perf_counter() - t_fill
     _log(f"cache filled ({w.total_tokens} tokens) in {t_fill:.1f} s")
     stream = torch.cuda.current_stream()
@@ -697,7 +706,8 @@ def main():
         ev[k][1].record(stream)
         run.decode()
         ev[k][2].record(stream)
-        run.combine()
+        if run.needs_combine:
+            run.combine()
         ev[k][3].record(stream)
     torch.cuda.synchronize()
     step_each = np.array([e[0].elapsed_time(e[3]) for e in ev]) * 1e3
@@ -728,7 +738,7 @@ def main():
         _log(f"cold: median {cold['median_us']} us, p90 {cold['p90_us']} us")
 
     # ---- the exact-accumulation QK mode, same cache, same plan ----------------
-    run_x = DecodeRunner(w, num_splits=run.num_splits, out_dtype=torch.bfloat16,
+    run_x = DecodeRunner(w, num_splits=run.num_splits, kv_chunk_tokens=run.kv_chunk_tokens, out_dtype=torch.bfloat16,
                          cache=(run.kv_latent, run.kv_scale, run.k_rope), exact_qk=True)
     for _ in range(args.warmup):
         run_x.step()
@@ -793,7 +803,8 @@ def main():
             "ctx_min": int(w.seq_lens.min()), "ctx_max": int(w.seq_lens.max()),
             "kv_tokens": w.total_tokens, "kv_bytes": kv_bytes, "page": 64,
             "num_splits": run.num_splits, "kv_chunk_tokens": run.kv_chunk_tokens,
-            "append_per_step": w.n_new, "step": "append + decode + combine",
+            "append_per_step": w.n_new,
+            "step": "append + decode + combine" if run.needs_combine else "append + decode (unsplit plan, rows written by the decode)",
         },
         "us_per_step_graph": round(graph_us, 1),
         "breakdown_us": {"append": round(append_us, 2), "decode": round(decode_us, 2),

@@ -25,6 +25,29 @@ def _u16_to_bf16(a):
     return t.view(torch.bfloat16)
 
 
+# A period (one 64-token block) of a decode workgroup takes ~2 us; a combine launch
+# costs about as much as four of them on a small batch (measured on 1 x 256 tokens:
+# 27.4 us per step with 8 parts + combine, 21.7 us with one piece and no combine).
+UNSPLIT_SLACK_BLOCKS = 4
+
+
+def prefer_unsplit(seq_lens, q_len, H, kv_dtype="e4m3", device=None):
+    """Whether the unsplit plan (one piece per sequence, rows written by the decode, no combine) is
+    expected to be faster than the balanced split + combine: every sequence's workgroups fit on the
+    chip at once, the longest sequence holds at most UNSPLIT_SLACK_BLOCKS more blocks than a part of
+    the balanced plan, and the decode writes direct rows for this shape (the FP8-cache decode with one
+    64-row group, the BF16-cache decode always)."""
+    groups = (q_len * H + 63) // 64
+    if kv_dtype != "bf16" and groups > 1:
+        return False
+    props = torch.cuda.get_device_properties(device if device is not None else torch.cuda.current_device())
+    blocks = (np.asarray(seq_lens, np.int64) + PAGE - 1) // PAGE
+    if len(blocks) == 0 or len(blocks) * groups > props.multi_processor_count:
+        return False
+    parts = sm.default_num_splits(q_len, H, device=device, total_blocks=int(blocks.sum()))
+    return int(blocks.max()) <= blocks.sum() / parts + UNSPLIT_SLACK_BLOCKS
+
+
 class DecodeRunner:
     """Holds one workload's device buffers.
 
@@ -40,12 +63,16 @@ class DecodeRunner:
         exact_qk: decode with SNAPMLA_DECODE_EXACT_QK (content term accumulated exactly in float32).
         direct: the decode writes the rows of sequences that one piece covers into out/lse itself
         (False: partials only, every row from the combine).  unsplit: one piece per sequence (fixed
-        chunks as long as the page table, one split), so that the step needs no combine."""
+        chunks as long as the page table, one split), so that the step needs no combine; "auto": that plan
+        when prefer_unsplit expects it to be faster and no plan is given."""
         self.kv_dtype = kv_dtype
         self.flags = sm.DECODE_EXACT_QK if exact_qk else 0
         self.wl = wl
         self.B, self.H, self.q_len = wl.B, wl.H, wl.q_len
         self.direct = direct
+        if unsplit == "auto":
+            unsplit = num_splits is None and kv_chunk_tokens is None and wl.kv_chunk_tokens == 0 and \
+                prefer_unsplit(wl.seq_lens, wl.q_len, wl.H, kv_dtype)
         if unsplit:
             kv_chunk_tokens, num_splits = wl.max_pages * PAGE, 1
         self.kv_chunk_tokens = wl.kv_chunk_tokens if kv_chunk_tokens is None else kv_chunk_tokens

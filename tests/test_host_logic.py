@@ -40,3 +40,18 @@ def sm(monkeypatch):
 ])
 def test_default_num_splits(sm, q_len, H, blocks, expect):
     assert sm.default_num_splits(q_len, H, total_blocks=blocks) == expect
+
+
+@pytest.mark.parametrize("lens,q_len,H,kv,expect", [
+    ([256], 1, 16, "e4m3", True),                 # 4 blocks on 8 parts: one piece, no combine
+    ([1024] * 256, 1, 64, "e4m3", True),          # every sequence one part's worth, 256 workgroups
+    ([1024] * 257, 1, 64, "e4m3", False),         # more workgroups than CUs
+    ([4096] * 32, 1, 64, "e4m3", False),          # 64 blocks per sequence against 8 per part
+    ([256], 1, 128, "e4m3", False),               # two row groups: no direct rows in the FP8 decode
+    ([256], 1, 128, "bf16", True),                # the BF16 decode writes them with any row count
+    ([64 * 4, 64], 1, 64, "e4m3", True),          # 4 blocks against 5/8 + 4
+    ([64 * 4 + 1, 64], 1, 64, "e4m3", False),     # 5 blocks against 6/8 + 4: beyond the slack
+])
+def test_prefer_unsplit(sm, lens, q_len, H, kv, expect):
+    from paper_2602_10718_amd import runner
+    assert runner.prefer_unsplit(lens, q_len, H, kv) == expect
