@@ -376,14 +376,13 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
           sk[i] = vis_j ? sk[i] : 0.0f;
         }
       }
-      float mt = fmaxf(fmaxf(fmaxf(pp[0], pp[1]), fmaxf(pp[2], pp[3])), fmaxf(fmaxf(pp[4], pp[5]), fmaxf(pp[6], pp[7])));
-      mt = fmaxf(mt, fmaxf(fmaxf(fmaxf(pp[8], pp[9]), fmaxf(pp[10], pp[11])),
-                           fmaxf(fmaxf(pp[12], pp[13]), fmaxf(pp[14], pp[15]))));
-      const float mb = quad_max(mt) * sl2;         // block max of this row (log2 units)
+      // (maxima that propagate NaN: no logit is NaN here -- hidden and stale slots are -inf,
+      // and a bad page marks the piece NaN whatever its logits)
+      const float mb = quad_vmax(vmax16(pp)) * sl2;  // block max of this row (log2 units)
       v4i mine = v4i{0, 0, 0, 0};
       float gam = 1.0f;
       if (likely(mb > -INFINITY)) {                        // the row sees a token of this block
-        const float m_new = fmaxf(m, mb);
+        const float m_new = vmax(m, mb);
         float e[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) e[i] = __builtin_amdgcn_exp2f(fmaf(pp[i], sl2, -m_new));
@@ -391,11 +390,9 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         for (int i = 0; i < 16; ++i) pp[i] = e[i] * sk[i];
         float esum = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
         esum += ((e[8] + e[9]) + (e[10] + e[11])) + ((e[12] + e[13]) + (e[14] + e[15]));
-        float pmax = fmaxf(fmaxf(fmaxf(pp[0], pp[1]), fmaxf(pp[2], pp[3])), fmaxf(fmaxf(pp[4], pp[5]), fmaxf(pp[6], pp[7])));
-        pmax = fmaxf(pmax, fmaxf(fmaxf(fmaxf(pp[8], pp[9]), fmaxf(pp[10], pp[11])),
-                                 fmaxf(fmaxf(pp[12], pp[13]), fmaxf(pp[14], pp[15]))));
+        float pmax = vmax16(pp);
         esum = quad_sum(esum);
-        pmax = quad_max(pmax);
+        pmax = quad_vmax(pmax);
         // (reciprocals instead of divisions: off by at most an ulp, far inside the
         // rounding slack of the probability codes)
         const float sP = fmaxf(pmax * (1.0f / kFp8Max), kEps);

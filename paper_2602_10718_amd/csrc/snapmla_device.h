@@ -105,6 +105,26 @@ __device__ __forceinline__ float quad_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// The same maximum with NaN-propagating semantics (v_maximum3_f32 on gfx950): no
+// quieting of signalling NaNs is needed first, so reductions over values the compiler
+// cannot prove canonical (lane swaps, merged branches) take one instruction per pair
+// or triple.  For callers whose inputs hold no NaN (masked slots are -inf), the result
+// equals fmaxf's.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float vmax3(float a, float b, float c) { return vmax(vmax(a, b), c); }
+__device__ __forceinline__ float quad_vmax(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+// max over 16 values as five three-input maxima
+__device__ __forceinline__ float vmax16(const float (&v)[16]) {
+  const float a = vmax3(v[0], v[1], v[2]), b = vmax3(v[3], v[4], v[5]), c = vmax3(v[6], v[7], v[8]);
+  const float d = vmax3(v[9], v[10], v[11]), e = vmax3(v[12], v[13], v[14]);
+  return vmax(vmax3(a, b, c), vmax3(d, e, v[15]));
+}
+
 __device__ __forceinline__ float wave_max(float x) {
   for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
   return x;
