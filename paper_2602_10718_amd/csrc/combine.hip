@@ -3,10 +3,18 @@
 // Each KV piece p of a sequence delivered a normalized partial output o_p and its
 // log-sum-exp LSE_p (Algorithm 1 returns both per query row).  Per row:
 //   LSE = log sum_p exp(LSE_p),   o = sum_p exp(LSE_p - LSE) * o_p.
-// One wave merges one row; lane l owns output dimensions 8l..8l+7.  The pieces'
-// log-sum-exps are read lane-parallel and the partial rows four at a time.
 // When the decode was given the output (ctrl[0] == 1) it has written the rows of
 // every sequence that at most one piece covers; those are left as they are.
+//
+// Two kernels, one per slot layout (part_tile_offset):
+// - one row group (plain rows): one wave per row; lane l owns output dimensions
+//   8l..8l+7.  The pieces' log-sum-exps are read lane-parallel, and a piece whose
+//   weight underflows to zero is not read at all (the row's partial sits in its own
+//   cache lines).
+// - several row groups (tile order): one wave per 32-row x 32-dimension tile, lane
+//   n + 32h on row n of the tile, dimensions 8q + 4h .. +3; every partial load of a
+//   wave reads 1 KiB of consecutive bytes.  Each lane merges its row with a running
+//   maximum, four pieces per round so that their loads overlap.
 
 #include "piece_end.h"
 #include "snapmla_device.h"
@@ -14,38 +22,53 @@
 
 namespace snapmla {
 
-__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+// The pieces of sequence b: candidates first..last; exists(i) rejects an empty part
+// (only possible with fewer blocks than parts), pid(i) is the piece's slot.
+// Balanced plan: part w covers global blocks [w*TB/W, (w+1)*TB/W) and writes piece
+// id w + b for every sequence b it touches; fixed chunks: piece id b*W + chunk.
+// (a sequence with blocks meets only non-empty parts, so last - first + 1 is its
+// piece count)
+struct Pieces {
+  int first = 0, last = -1, b = 0, W = 1;
+  bool balanced = true;
+  int64_t TB = 0;
+  __device__ bool exists(int i) const {
+    return !balanced || TB >= W || (int64_t)i * TB / W < (int64_t)(i + 1) * TB / W;
+  }
+  __device__ int64_t pid(int i) const { return balanced ? (int64_t)i + b : (int64_t)b * W + i; }
+};
+
+__device__ Pieces pieces_of(const CombineArgs& a, int b) {
+  Pieces P;
+  P.b = b;
+  P.W = a.num_splits;
+  P.balanced = a.chunk_blocks == 0;
+  P.TB = a.prefix[a.B];
+  const int p0 = a.prefix[b], p1 = a.prefix[b + 1];
+  const int nb = p1 - p0;
+  if (nb > 0) {
+    if (P.balanced) {
+      P.first = (int)(((int64_t)(p0 + 1) * P.W - 1) / P.TB);
+      P.last = (int)(((int64_t)p1 * P.W - 1) / P.TB);
+    } else {
+      P.first = 0;
+      P.last = (nb + a.chunk_blocks - 1) / a.chunk_blocks - 1;
+    }
+  }
+  return P;
+}
+
+__global__ __launch_bounds__(256) void combine_rows_kernel(CombineArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t wv = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (wv >= (int64_t)a.B * a.R) return;
   const int b = (int)(wv / a.R), r = (int)(wv % a.R);
 
-  const int p0 = a.prefix[b], p1 = a.prefix[b + 1];
-  const int nb = p1 - p0;
-  const bool balanced = a.chunk_blocks == 0;
-  const int64_t T = a.prefix[a.B];
-  const int W = a.num_splits;
-  // balanced plan: part w covers global blocks [w*T/W, (w+1)*T/W) and writes piece
-  // id w + b for every sequence b it touches; fixed chunks: piece id b*W + chunk.
-  // [first, last] is the candidate range; `exists` rejects empty parts.
-  int first = 0, last = -1;
-  if (nb > 0) {
-    if (balanced) {
-      first = (int)(((int64_t)(p0 + 1) * W - 1) / T);
-      last = (int)(((int64_t)p1 * W - 1) / T);
-    } else {
-      first = 0;
-      last = (nb + a.chunk_blocks - 1) / a.chunk_blocks - 1;
-    }
-  }
-  // (a sequence with blocks meets only non-empty parts, so last - first + 1 is its
-  // piece count)
+  const Pieces P = pieces_of(a, b);
+  const int first = P.first, last = P.last;
   if (a.ctrl[0] == 1 && last <= first) return;
-  auto exists = [&](int i) -> bool {
-    if (!balanced) return true;
-    return (int64_t)i * T / W < (int64_t)(i + 1) * T / W;
-  };
-  auto pid = [&](int i) -> int64_t { return balanced ? (int64_t)i + b : (int64_t)b * W + i; };
+  auto exists = [&](int i) { return P.exists(i); };
+  auto pid = [&](int i) { return P.pid(i); };
 
   // pass 1: lane i reads the log-sum-exp of candidate piece first + i (64 at a
   // time), the wave reduces the maximum and NaN flag
@@ -129,12 +152,105 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   if (a.lse != nullptr && lane == 0) a.lse[orow] = lse;
 }
 
+__global__ __launch_bounds__(256) void combine_tiles_kernel(CombineArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int n = lane & 31, h = lane >> 5;
+  const int T = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tiles = (a.R + 31) / 32;                 // 32-row tiles per sequence
+  const int dq = (int)(blockIdx.x & 3);
+  const int64_t bt = blockIdx.x >> 2;
+  const int b = (int)(bt / tiles), t = (int)(bt % tiles);
+  const int row = 32 * t + n;                        // query row of this lane (< rows_pad)
+
+  const Pieces P = pieces_of(a, b);
+  const int first = P.first, last = P.last;
+  if (a.ctrl[0] == 1 && last <= first) return;
+  auto exists = [&](int i) { return P.exists(i); };
+  auto pid = [&](int i) { return P.pid(i); };
+  const int64_t tile = part_tile_offset(t >> 1, dq, t & 1, T, 0, lane);
+
+  // this wave's pieces, merged with a running maximum M: S = sum exp(LSE_i - M),
+  // acc = sum exp(LSE_i - M) o_i.  Every row of an existing piece's slot was written
+  // (0 for a row without tokens, NaN for a rejected piece).
+  float M = -INFINITY, S = 0.0f;
+  bool anynan = false;
+  v4f acc[4] = {v4f{0.f, 0.f, 0.f, 0.f}, v4f{0.f, 0.f, 0.f, 0.f}, v4f{0.f, 0.f, 0.f, 0.f}, v4f{0.f, 0.f, 0.f, 0.f}};
+  for (int i0 = first; i0 <= last; i0 += 4) {
+    float x[4];
+    v4f u[4][4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = i0 + j;
+      const bool live = i <= last && exists(i);
+      const int64_t p = pid(live ? i : first);       // in range even when unused
+      x[j] = live ? a.part_lse[p * a.rows_pad + row] : -INFINITY;
+      const v4f* src = reinterpret_cast<const v4f*>(a.part_o + p * a.rows_pad * kDc + tile);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) u[j][q] = live ? src[64 * q] : v4f{0.f, 0.f, 0.f, 0.f};
+    }
+    float mr = M;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      anynan |= x[j] != x[j];
+      mr = fmaxf(mr, x[j]);
+    }
+    if (mr > -INFINITY) {
+      const float sc = expf(M - mr);                 // 0 while M is -inf
+      S *= sc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[q] *= sc;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float wj = x[j] > -INFINITY ? expf(x[j] - mr) : 0.0f;
+        S += wj;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[q] += wj * u[j][q];
+      }
+      M = mr;
+    }
+  }
+  if (row >= a.R) return;
+  const bool bad = a.flags[b] != 0 || anynan;
+  v4f o[4];
+  float lse;
+  if (bad) {
+    const float nanv = __builtin_nanf("");
+    for (int q = 0; q < 4; ++q) o[q] = v4f{nanv, nanv, nanv, nanv};
+    lse = nanv;
+  } else if (!(M > -INFINITY)) {
+    for (int q = 0; q < 4; ++q) o[q] = v4f{0.f, 0.f, 0.f, 0.f};
+    lse = -INFINITY;
+  } else {
+    const float inv = 1.0f / S;
+    for (int q = 0; q < 4; ++q) o[q] = acc[q] * inv;
+    lse = M + logf(S);
+  }
+  const int64_t orow = (int64_t)b * a.R + row;
+  const int64_t col = 128 * dq + 32 * T + 4 * h;
+  for (int q = 0; q < 4; ++q) {
+  if (a.out_dtype == 1) {
+    *reinterpret_cast<v4f*>(reinterpret_cast<float*>(a.out) + orow * kDc + col + 8 * q) = o[q];
+  } else {
+    const uint32_t lo = f32_to_bf16_bits(o[q][0]) | (f32_to_bf16_bits(o[q][1]) << 16);
+    const uint32_t hi = f32_to_bf16_bits(o[q][2]) | (f32_to_bf16_bits(o[q][3]) << 16);
+    *reinterpret_cast<v2i*>(reinterpret_cast<uint16_t*>(a.out) + orow * kDc + col + 8 * q) = v2i{(int)lo, (int)hi};
+  }
+  }
+  if (a.lse != nullptr && dq == 0 && T == 0 && h == 0) a.lse[orow] = lse;
+}
+
 hipError_t launch_combine(const CombineArgs& a, hipStream_t stream) {
-  const int64_t waves = (int64_t)a.B * a.R;
-  if (waves <= 0) return hipSuccess;
-  const int64_t blocks = (waves + 3) / 4;
-  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+  if ((int64_t)a.B * a.R <= 0) return hipSuccess;
+  if (a.rows_pad > 64) {
+    // one workgroup per sequence, 32-row tile and 128-dimension quarter
+    const int64_t blocks = (int64_t)a.B * ((a.R + 31) / 32) * 4;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(combine_tiles_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+  } else {
+    const int64_t blocks = ((int64_t)a.B * a.R + 3) / 4;   // one wave per row
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(combine_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

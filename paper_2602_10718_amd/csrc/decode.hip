@@ -566,17 +566,18 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         stored = false;
         if (likely(k > 0)) {
           // ---- PV of block k-1 --------------------------------------------------
-  #pragma unroll
-          for (int T = 0; T < 4; ++T) {
-            O[2 * T] *= gl0[0];
-            O[2 * T + 1] *= gl1[0];
-          }
+          // each accumulator is rescaled right before its product, so that the
+          // multiplies of the next one run while the matrix core works
   #pragma unroll
           for (int T = 0; T < 4; ++T) {
             const v8i A = v8i{rv[T][0][0], rv[T][0][1], rv[T][1][0], rv[T][1][1],
                               rv[T][2][0], rv[T][2][1], rv[T][3][0], rv[T][3][1]};
+            O[2 * T] *= gl0[0];
             O[2 * T] = mfma_f8_32x32x64(A, P0, O[2 * T]);
+            __builtin_amdgcn_sched_barrier(0);
+            O[2 * T + 1] *= gl1[0];
             O[2 * T + 1] = mfma_f8_32x32x64(A, P1, O[2 * T + 1]);
+            __builtin_amdgcn_sched_barrier(0);
           }
           // ---- end of a piece: write the normalized partial output and LSE ----
           // (one 16-byte store at a time; a bad page id makes the multiplier NaN)
@@ -731,11 +732,13 @@ __global__ __launch_bounds__(512, 1) void decode_kernel(DecodeArgs a, const int3
         // ---- PV of block k-1, then the V^T reads of block k ---------------------
         const uint32_t st_lds = smem_base + (k % kLatStages) * kLatBytes;
         auto pv_tile = [&](int T, v2i (&src)[4]) {
-          O[2 * T] *= gl0[0];
-          O[2 * T + 1] *= gl1[0];
           const v8i A = v8i{src[0][0], src[0][1], src[1][0], src[1][1], src[2][0], src[2][1], src[3][0], src[3][1]};
+          O[2 * T] *= gl0[0];
           O[2 * T] = mfma_f8_32x32x64(A, P0, O[2 * T]);
+          __builtin_amdgcn_sched_barrier(0);
+          O[2 * T + 1] *= gl1[0];
           O[2 * T + 1] = mfma_f8_32x32x64(A, P1, O[2 * T + 1]);
+          __builtin_amdgcn_sched_barrier(0);
         };
         auto tr_tile = [&](int T, v2i (&dst)[4]) {
   #pragma unroll

@@ -26,9 +26,12 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float x) {
 // A piece that covers its whole sequence (whole, with a.out set) is final: its rows
 // go to out[seq*R + row] in the output type and its LSEs to out_lse; otherwise the
 // normalized partial and its LSE go to the piece's slot pid of the workspace, which
-// snapmla_combine merges.  Rows from R up to rows_pad (padding of the last row group)
-// always go to the slot, which holds rows_pad rows and is never read for them: the
-// store count stays the same whatever the destination.
+// snapmla_combine merges.  With several row groups the slot is in accumulator tile
+// order (part_tile_offset: each store instruction writes 1 KiB of consecutive bytes),
+// with one it holds plain rows (32 bytes in each of 32 rows per instruction).  Rows
+// from R up to rows_pad (padding of the last row group) always go to the slot, which
+// holds rows_pad rows and is never read for them: the store count stays the same
+// whatever the destination.
 __device__ __forceinline__ void store_piece(const DecodeArgs& a, const v16f (&O)[8], float inv0, float inv1,
                                             float lse0, float lse1, int row0, int row1, int dq, int h,
                                             int64_t pid, int seq, bool whole) {
@@ -37,14 +40,20 @@ __device__ __forceinline__ void store_piece(const DecodeArgs& a, const v16f (&O)
   for (int r = 0; r < 2; ++r) {
     const int row = r == 0 ? row0 : row1;
     const float inv = r == 0 ? inv0 : inv1;
-    float* slot = a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
+    const bool tiles = a.rows_pad > 64;
+    float* slot = tiles ? a.part_o + pid * a.rows_pad * kDc + part_tile_offset(row >> 6, dq, r, 0, 0, (row & 31) + 32 * h)
+                        : a.part_o + (pid * a.rows_pad + row) * kDc + 128 * dq + 4 * h;
     float* slot_lse = a.part_lse + pid * a.rows_pad + row;
+    // float offsets of tile T, chunk pair q inside the slot (plain rows: 32T + 8q)
+    const int st = tiles ? 1024 : 32, sq = tiles ? 256 : 8;
     const bool mine = direct && row < a.R;
     const int64_t orow = (int64_t)seq * a.R + row;
     if (direct && a.out_dtype == 0) {
       // bf16 rows: four values (8 bytes) per store
+      // (a padding row writes its bf16 pairs into the first half of its slot cells)
       uint16_t* dst = mine ? static_cast<uint16_t*>(a.out) + orow * kDc + 128 * dq + 4 * h
                            : reinterpret_cast<uint16_t*>(slot);
+      const int bt = mine ? 32 : 2 * st, bq = mine ? 8 : 2 * sq;        // uint16 units
 #pragma unroll
       for (int T = 0; T < 4; ++T) {
 #pragma unroll
@@ -52,19 +61,20 @@ __device__ __forceinline__ void store_piece(const DecodeArgs& a, const v16f (&O)
           const v16f& o = O[2 * T + r];
           const uint32_t lo = f32_to_bf16_bits(o[4 * q + 0] * inv) | (f32_to_bf16_bits(o[4 * q + 1] * inv) << 16);
           const uint32_t hi = f32_to_bf16_bits(o[4 * q + 2] * inv) | (f32_to_bf16_bits(o[4 * q + 3] * inv) << 16);
-          *reinterpret_cast<v2i*>(dst + 32 * T + 8 * q) = v2i{(int)lo, (int)hi};
+          *reinterpret_cast<v2i*>(dst + bt * T + bq * q) = v2i{(int)lo, (int)hi};
           __builtin_amdgcn_sched_barrier(0);
         }
       }
     } else {
       // float32 rows (final or partial): four values (16 bytes) per store
       float* dst = mine ? static_cast<float*>(a.out) + orow * kDc + 128 * dq + 4 * h : slot;
+      const int ft = mine ? 32 : st, fq = mine ? 8 : sq;
 #pragma unroll
       for (int T = 0; T < 4; ++T) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const v16f& o = O[2 * T + r];
-          *reinterpret_cast<v4f*>(dst + 32 * T + 8 * q) =
+          *reinterpret_cast<v4f*>(dst + ft * T + fq * q) =
               v4f{o[4 * q + 0] * inv, o[4 * q + 1] * inv, o[4 * q + 2] * inv, o[4 * q + 3] * inv};
           __builtin_amdgcn_sched_barrier(0);
         }

@@ -74,7 +74,7 @@ struct DecodeArgs {
   const int32_t* prefix;
   const int32_t* desc;      // [units][kDescInts]
   const uint8_t* zero;
-  float* part_o;            // [pieces][rows_pad][512]
+  float* part_o;            // [pieces][rows_pad * 512]: rows, or part_tile_offset order (rows_pad > 64)
   float* part_lse;          // [pieces][rows_pad]
   int B, q_len, H, R, G, rows_pad, max_pages, num_pages, causal;
   int num_splits, chunk_blocks;  // chunk_blocks == 0: balanced plan over num_splits parts
@@ -101,6 +101,19 @@ __host__ __device__ inline bool seq_len_ok(int n, int q_len, int max_pages, int 
   bool ok = (n == 0) || (n >= q_len && (int64_t)n <= (int64_t)max_pages * 64);
   if (ok && chunk_blocks > 0) ok = ((n + 63) / 64 + chunk_blocks - 1) / chunk_blocks <= num_splits;
   return ok;
+}
+
+// Float32 offset of a partial-output element inside its piece's slot when the rows
+// form several 64-row groups (rows_pad > 64).  The order follows the PV waves'
+// accumulator tiles, so that each 16-byte store instruction of a wave writes 1 KiB of
+// consecutive memory: row group g (rows 64g..64g+63), dimension quarter dq (128
+// dimensions), row tile rt (32 rows), dimension tile T (32 dimensions), chunk pair q
+// (8 dimensions), then lane n + 32h, which holds row 64g + 32rt + n, dimensions
+// 128dq + 32T + 8q + 4h .. +3.  With one row group the slot keeps plain rows
+// ([64][512]): there the merge skips, row by row, the pieces whose weight underflows
+// to zero, which needs each row's partial in its own cache lines.
+__host__ __device__ constexpr int64_t part_tile_offset(int g, int dq, int rt, int T, int q, int lane) {
+  return (int64_t)g * 32768 + dq * 8192 + rt * 4096 + T * 1024 + q * 256 + lane * 4;
 }
 
 struct CombineArgs {
