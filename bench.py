@@ -47,9 +47,10 @@ def _log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-SOURCES_OF = {"decode": ("decode.hip", "quant.hip", "snapmla_device.h"),
+SOURCES_OF = {"decode": ("decode.hip", "quant.hip", "piece_end.h", "snapmla_device.h", "snapmla_internal.h"),
               "fetch_dequant": ("fetch.hip", "snapmla_device.h"),
-              "decode_bf16": ("decode_bf16.hip", "quant.hip", "snapmla_device.h")}
+              "decode_bf16": ("decode_bf16.hip", "quant.hip", "piece_end.h", "snapmla_device.h",
+                              "snapmla_internal.h")}
 
 
 def _src_hash(op="decode"):
