@@ -128,7 +128,8 @@ int snapmla_quantize_rows(const void* x, int64_t rows, uint8_t* codes, float* sc
 /*
  * Workspace for snapmla_decode / snapmla_combine, in bytes.  It holds the
  * quantized queries, the split plan and, per KV piece, a float32 partial
- * output [64*ceil(R/64)][512] and partial log-sum-exp.
+ * output of 64*ceil(R/64) rows x 512 (in an order of the library's own, read
+ * only by snapmla_combine) and partial log-sum-exp.
  *   kv_chunk_tokens == 0: balanced split over `num_splits` parts of the total
  *                         64-token block count (num_splits >= 1; a sequence
  *                         may span several parts and a part several sequences)
