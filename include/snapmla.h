@@ -132,7 +132,10 @@ int snapmla_quantize_rows(const void* x, int64_t rows, uint8_t* codes, float* sc
  * only by snapmla_combine) and partial log-sum-exp.
  *   kv_chunk_tokens == 0: balanced split over `num_splits` parts of the total
  *                         64-token block count (num_splits >= 1; a sequence
- *                         may span several parts and a part several sequences)
+ *                         may span several parts and a part several sequences;
+ *                         with R <= 64 each sequence start counts as 4 extra
+ *                         blocks, so parts that hold a sequence boundary get
+ *                         up to 4 fewer blocks)
  *   kv_chunk_tokens  > 0: every sequence is cut into chunks of kv_chunk_tokens
  *                         (a multiple of 64); num_splits bounds the chunks per
  *                         sequence (sequences needing more are flagged NaN).

@@ -132,6 +132,7 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
   p.zero = ws + L.zero;
   p.desc = reinterpret_cast<int32_t*>(ws + L.desc);
   p.units = L.units;
+  p.pad = L.pad;
   p.B = B;
   p.q_len = q_len;
   p.max_pages = max_pages;
@@ -210,6 +211,7 @@ WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens)
   L.zero = off;   off += 1024;
   L.ctrl = off;   off += 256;
   L.units = kv_chunk_tokens == 0 ? num_splits : B * num_splits;   // <= 2^26 (check_shapes)
+  L.pad = kv_chunk_tokens == 0 && L.G == 1 ? kPlanPad : 0;
   L.desc = off;   off += align256((size_t)L.units * kDescInts * 4);
   L.lse = off;    off += align256((size_t)L.pieces * L.rows_pad * 4);
   L.o = off;      off += align256((size_t)L.pieces * L.rows_pad * 512 * 4);
@@ -377,6 +379,7 @@ int snapmla_combine(const void* workspace, size_t workspace_bytes, const int32_t
   c.num_splits = num_splits;
   c.chunk_blocks = kv_chunk_tokens / 64;
   c.out_dtype = out_dtype;
+  c.pad = L.pad;
   return hip_status(snapmla::launch_combine(c, stream), "combine launch");
 }
 

@@ -23,17 +23,18 @@
 namespace snapmla {
 
 // The pieces of sequence b: candidates first..last; exists(i) rejects an empty part
-// (only possible with fewer blocks than parts), pid(i) is the piece's slot.
-// Balanced plan: part w covers global blocks [w*TB/W, (w+1)*TB/W) and writes piece
-// id w + b for every sequence b it touches; fixed chunks: piece id b*W + chunk.
-// (a sequence with blocks meets only non-empty parts, so last - first + 1 is its
-// piece count)
+// (only possible with fewer virtual positions than parts), pid(i) is the piece's slot.
+// Balanced plan: part w covers the real blocks of virtual positions [w*TV/W,
+// (w+1)*TV/W) (kPlanPad) and writes piece id w + b for every sequence b it touches;
+// fixed chunks: piece id b*W + chunk.  (The parts that meet sequence b's real blocks
+// are exactly those whose virtual range meets [prefix[b] + pad*(b+1), prefix[b+1] +
+// pad*(b+1)); each of them has a non-empty range, so last - first + 1 counts its pieces.)
 struct Pieces {
   int first = 0, last = -1, b = 0, W = 1;
   bool balanced = true;
-  int64_t TB = 0;
+  int64_t TV = 0;
   __device__ bool exists(int i) const {
-    return !balanced || TB >= W || (int64_t)i * TB / W < (int64_t)(i + 1) * TB / W;
+    return !balanced || TV >= W || (int64_t)i * TV / W < (int64_t)(i + 1) * TV / W;
   }
   __device__ int64_t pid(int i) const { return balanced ? (int64_t)i + b : (int64_t)b * W + i; }
 };
@@ -43,13 +44,14 @@ __device__ Pieces pieces_of(const CombineArgs& a, int b) {
   P.b = b;
   P.W = a.num_splits;
   P.balanced = a.chunk_blocks == 0;
-  P.TB = a.prefix[a.B];
+  P.TV = a.prefix[a.B] + (int64_t)a.pad * a.B;
   const int p0 = a.prefix[b], p1 = a.prefix[b + 1];
   const int nb = p1 - p0;
   if (nb > 0) {
     if (P.balanced) {
-      P.first = (int)(((int64_t)(p0 + 1) * P.W - 1) / P.TB);
-      P.last = (int)(((int64_t)p1 * P.W - 1) / P.TB);
+      const int64_t v0 = p0 + (int64_t)a.pad * (b + 1);    // virtual position of the first block
+      P.first = (int)(((v0 + 1) * P.W - 1) / P.TV);
+      P.last = (int)(((v0 + nb) * P.W - 1) / P.TV);
     } else {
       P.first = 0;
       P.last = (nb + a.chunk_blocks - 1) / a.chunk_blocks - 1;

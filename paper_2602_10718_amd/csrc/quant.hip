@@ -139,8 +139,22 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
       int32_t* d = a.desc + (int64_t)u * kDescInts;
       int gs = 0, ge = 0, b = 0;
       if (a.chunk_blocks == 0) {
-        gs = (int)((int64_t)u * T / a.num_splits);
-        ge = (int)((int64_t)(u + 1) * T / a.num_splits);
+        // virtual positions (kPlanPad): sequence b's real blocks follow its pad empty
+        // positions; real(v) = the real blocks before virtual position v
+        const int64_t TV = (int64_t)T + (int64_t)a.pad * a.B;
+        auto real = [&](int64_t v) -> int {
+          if (a.pad == 0) return (int)v;
+          int lo = 0, hi = a.B - 1;                  // largest b with its virtual start <= v
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int64_t)pref(mid) + (int64_t)a.pad * mid <= v) lo = mid; else hi = mid - 1;
+          }
+          const int p0 = pref(lo);
+          const int64_t r = v - (p0 + (int64_t)a.pad * lo) - a.pad;
+          return p0 + (int)(r < 0 ? 0 : min<int64_t>(r, pref(lo + 1) - p0));
+        };
+        gs = real((int64_t)u * TV / a.num_splits);
+        ge = real((int64_t)(u + 1) * TV / a.num_splits);
         if (gs < ge) {                               // largest b with prefix[b] <= gs
           int lo = 0, hi = a.B - 1;
           while (lo < hi) {

@@ -11,9 +11,19 @@ namespace snapmla {
 struct WsLayout {
   int R = 0, G = 0, rows_pad = 0, pieces = 0;
   int units = 0;
+  int pad = 0;              // balanced plan: virtual blocks charged to each sequence start
   size_t q8 = 0, sq = 0, prefix = 0, flags = 0, zero = 0, ctrl = 0, desc = 0, lse = 0, o = 0, total = 0;
 };
 WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens);
+
+// Balanced plan: part u covers the real blocks of the virtual block positions
+// [u*TV/W, (u+1)*TV/W), TV = T + pad*B, where sequence b occupies the virtual positions
+// [prefix[b] + pad*b, prefix[b+1] + pad*(b+1)) with its pad leading positions empty.
+// A part that holds a sequence start so gets up to pad fewer blocks: a range that
+// crosses into another sequence pays a piece end and a piece start mid-range (~2.7
+// blocks' time with one row group).  With several row groups the period is the waves'
+// own work and equal block counts are kept (pad 0).
+constexpr int kPlanPad = 4;
 
 struct PrepArgs {
   const uint16_t* q_nope;   // [B*R][512]
@@ -26,6 +36,7 @@ struct PrepArgs {
   uint8_t* zero;            // 1 KiB that the decode kernel reads in place of slots past a sequence end
   int32_t* desc;            // [units][kDescInts] start descriptor of each split unit (see kDesc*)
   int B, q_len, max_pages, chunk_blocks, num_splits, units;
+  int pad = 0;              // balanced plan's virtual blocks per sequence start (WsLayout::pad)
   // Final results written by the decode itself (out != nullptr): the rows of sequences
   // without blocks (empty: o = 0, LSE = -inf; rejected by a data error: NaN), written by
   // the row waves, and ctrl[0] = 1, which tells the combine that the decode also wrote
@@ -126,6 +137,7 @@ struct CombineArgs {
   void* out;
   float* lse;
   int B, q_len, H, R, rows_pad, num_splits, chunk_blocks, out_dtype;
+  int pad;                  // balanced plan's virtual blocks per sequence start (WsLayout::pad)
 };
 
 struct FetchArgs {
