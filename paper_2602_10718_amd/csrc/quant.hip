@@ -101,6 +101,8 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   if (blockIdx.x == 0) {
     __shared__ int sums[256];
     __shared__ int lens[256];
+    __shared__ int wsum[4];
+    __shared__ int useq[kPlanTable + 1];
     const int per = (a.B + 255) / 256;
     const int b0 = tid * per, b1 = min(a.B, b0 + per);
     int local = 0;
@@ -112,20 +114,28 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
       a.flags[b] = ok ? 0 : 1;
       local += ok ? nb : 0;
     }
-    sums[tid] = local;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {      // inclusive Hillis-Steele scan
-      const int v = tid >= off ? sums[tid - off] : 0;
-      __syncthreads();
-      sums[tid] += v;
-      __syncthreads();
+    // inclusive scan of the per-thread block counts: within each wave, then the four
+    // wave totals
+    int incl = local;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += v;
     }
-    int run = tid > 0 ? sums[tid - 1] : 0;
+    if (lane == 63) wsum[tid >> 6] = incl;
+    __syncthreads();
+    for (int i = 0; i < (tid >> 6); ++i) incl += wsum[i];
+    sums[tid] = incl;
     if (tid == 0) a.prefix[0] = 0;
-    for (int b = b0; b < b1; ++b) {
-      const int n = a.seq_lens[b];
-      run += a.flags[b] ? 0 : (n + kPage - 1) / kPage;
-      a.prefix[b + 1] = run;
+    if (per == 1) {
+      if (tid < a.B) a.prefix[tid + 1] = incl;      // one sequence per thread: the scan is the prefix
+    } else {
+      int run = incl - local;
+      for (int b = b0; b < b1; ++b) {
+        const int n = a.seq_lens[b];
+        run += a.flags[b] ? 0 : (n + kPage - 1) / kPage;
+        a.prefix[b + 1] = run;
+      }
     }
     reinterpret_cast<uint32_t*>(a.zero)[tid] = 0u;   // 256 threads x 4 B = 1 KiB
     if (tid == 0) a.ctrl[0] = a.out != nullptr ? 1 : 0;
@@ -135,33 +145,61 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
     // (with one sequence per thread, B <= 256, the scan's LDS sums are the prefix)
     const int T = sums[255];
     auto pref = [&](int i) { return per == 1 ? (i == 0 ? 0 : sums[i - 1]) : a.prefix[i]; };
+    auto seq_of_block = [&](int gb) {                // largest b with prefix[b] <= gb
+      int lo = 0, hi = a.B - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (pref(mid) <= gb) lo = mid; else hi = mid - 1;
+      }
+      return lo;
+    };
+    // balanced plan over virtual positions (kPlanPad): sequence b spans [V_b, V_b+1),
+    // V_b = prefix[b] + pad*b, its real blocks after its first pad positions
+    const int W = a.num_splits;
+    const int64_t TV = (int64_t)T + (int64_t)a.pad * a.B;
+    auto vstart = [&](int b) { return (int64_t)pref(b) + (int64_t)a.pad * b; };
+    auto real_in = [&](int b, int64_t v) {           // real blocks before v, v in b's span
+      const int p0 = pref(b);
+      const int64_t r = v - vstart(b) - a.pad;
+      return p0 + (int)(r < 0 ? 0 : min<int64_t>(r, pref(b + 1) - p0));
+    };
+    // with few enough units, every sequence (one per thread) marks the units whose
+    // virtual start falls in its span: u with ceil(V_b W / TV) <= u < ceil(V_b+1 W / TV)
+    const bool table = a.chunk_blocks == 0 && per == 1 && a.units <= kPlanTable && TV > 0;
+    if (table) {
+      if (tid < a.B) {
+        const int ulo = (int)((vstart(tid) * W + TV - 1) / TV);
+        const int uhi = (int)((vstart(tid + 1) * W + TV - 1) / TV);
+        for (int u = ulo; u < uhi; ++u) useq[u] = tid;
+      }
+      __syncthreads();
+    }
     for (int u = tid; u < a.units; u += 256) {
       int32_t* d = a.desc + (int64_t)u * kDescInts;
       int gs = 0, ge = 0, b = 0;
       if (a.chunk_blocks == 0) {
-        // virtual positions (kPlanPad): sequence b's real blocks follow its pad empty
-        // positions; real(v) = the real blocks before virtual position v
-        const int64_t TV = (int64_t)T + (int64_t)a.pad * a.B;
-        auto real = [&](int64_t v) -> int {
-          if (a.pad == 0) return (int)v;
-          int lo = 0, hi = a.B - 1;                  // largest b with its virtual start <= v
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if ((int64_t)pref(mid) + (int64_t)a.pad * mid <= v) lo = mid; else hi = mid - 1;
+        if (TV > 0) {
+          const int64_t vs = (int64_t)u * TV / W, ve = (int64_t)(u + 1) * TV / W;
+          int bs, be;
+          if (table) {
+            bs = useq[u];
+            be = u + 1 < W ? useq[u + 1] : a.B - 1;
+          } else {                                   // largest b with V_b <= v
+            auto seq_of_v = [&](int64_t v) {
+              int lo = 0, hi = a.B - 1;
+              while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (vstart(mid) <= v) lo = mid; else hi = mid - 1;
+              }
+              return lo;
+            };
+            bs = seq_of_v(vs);
+            be = seq_of_v(ve);
           }
-          const int p0 = pref(lo);
-          const int64_t r = v - (p0 + (int64_t)a.pad * lo) - a.pad;
-          return p0 + (int)(r < 0 ? 0 : min<int64_t>(r, pref(lo + 1) - p0));
-        };
-        gs = real((int64_t)u * TV / a.num_splits);
-        ge = real((int64_t)(u + 1) * TV / a.num_splits);
-        if (gs < ge) {                               // largest b with prefix[b] <= gs
-          int lo = 0, hi = a.B - 1;
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (pref(mid) <= gs) lo = mid; else hi = mid - 1;
-          }
-          b = lo;
+          gs = real_in(bs, vs);
+          ge = real_in(be, ve);
+          // block gs lies in sequence bs unless bs has no blocks
+          if (gs < ge) b = pref(bs + 1) > gs ? bs : seq_of_block(gs);
         }
       } else {
         b = u / a.num_splits;

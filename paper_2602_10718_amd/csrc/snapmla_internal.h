@@ -24,6 +24,8 @@ WsLayout ws_layout(int B, int q_len, int H, int num_splits, int kv_chunk_tokens)
 // blocks' time with one row group).  With several row groups the period is the waves'
 // own work and equal block counts are kept (pad 0).
 constexpr int kPlanPad = 4;
+// units up to which the prep kernel maps units to sequences through an LDS table
+constexpr int kPlanTable = 1024;
 
 struct PrepArgs {
   const uint16_t* q_nope;   // [B*R][512]
