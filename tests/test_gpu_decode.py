@@ -154,6 +154,29 @@ def test_plan_with_many_sequences_and_units():
             check_sequence(run, b, reference(w, b, qn, qr), label=f"many-seq {kw}")
 
 
+@pytest.mark.parametrize("splits", [600, 1024, 1500])
+def test_padded_plan_with_more_parts_than_positions(splits):
+    """The balanced plan of a one-row-group launch charges each sequence start 4 virtual
+    blocks.  With short sequences and many parts, most parts fall inside those charges and
+    get no blocks; 600 and 1,024 parts take the prep kernel's unit table, 1,500 its binary
+    searches.  Every sequence must still come out whole: empty ones 0 / -inf, the others
+    equal to the oracle."""
+    rng = np.random.default_rng(37)
+    lens = rng.integers(1, 200, 200).astype(np.int32)
+    lens[[3, 64, 65, 199]] = 0                              # empty sequences, one of them last
+    w = wl.custom(B=200, H=16, q_len=1, seq_lens=lens.tolist(), seed=37)
+    qn, qr = w.queries()
+    run = _run(w, num_splits=splits)
+    print(f"[padded plan] splits={splits} blocks={int(((lens + 63) // 64).sum())}", flush=True)
+    out = run.out.cpu().numpy()
+    lse = run.lse.cpu().numpy()
+    assert np.all(np.isfinite(out)), "non-finite output"
+    for b in (3, 64, 65, 199):
+        assert np.all(out[b] == 0) and np.all(lse[b] == -np.inf)
+    for b in (0, 1, 2, 4, 63, 66, 100, 150, 197, 198):
+        check_sequence(run, b, reference(w, b, qn, qr), label=f"padded plan {splits}")
+
+
 @pytest.mark.parametrize("name", ["ragged-h16", "h128-two-rowgroups", "mtp-causal-r256", "fixed-chunks-causal"])
 def test_append_decode_equals_separate_calls(name):
     """snapmla_append_decode (append inside the preparation launch) against snapmla_quantize_append
