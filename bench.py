@@ -60,8 +60,9 @@ def _src_hash(op="decode"):
     return h.hexdigest()[:16]
 
 
-def _traffic(key, op="decode"):
-    """HBM bytes per launch measured with rocprofv3 counters (profiles/), if the sources still match."""
+def _traffic(key, op="decode", kernel=None):
+    """HBM bytes per launch measured with rocprofv3 counters (profiles/), if the sources still match: of the
+    whole call, or of one of its kernels (read + written)."""
     try:
         d = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
@@ -69,6 +70,9 @@ def _traffic(key, op="decode"):
     e = d.get(key)
     if not e or e.get("src_hash") != _src_hash(op):
         return None
+    if kernel is not None:
+        k = e.get(kernel)
+        return None if not k else k["read"] + k["write"]
     return e.get("hbm_bytes_per_launch")
 
 
@@ -717,6 +721,11 @@ def main():
     combine_us = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e3
     _log(f"per call: append {append_us:.1f} decode {decode_us:.1f} combine {combine_us:.1f} us")
 
+    # ---- the decode kernel alone: the decode launch without its preparation launch,
+    # over the workspace the calls above prepared (the dominant kernel of the roofline)
+    kernel_us = timed(run.decode_kernel_only, args.steps) * 1e3
+    _log(f"decode kernel alone: {kernel_us:.1f} us")
+
     # ---- cold cache: 1 GiB scratch write + read between steps (not timed) ----
     cold = None
     if args.cold_steps > 0:
@@ -761,27 +770,37 @@ def main():
 
     gbps = kv_bytes / (ms_per_step * 1e-3) / 1e9
     decode_gbps = kv_bytes / (decode_us * 1e-6) / 1e9
+    kernel_gbps = kv_bytes / (kernel_us * 1e-6) / 1e9
     ceiling["decode_call_frac"] = round(ceiling["us"] / decode_us, 4)
-    traffic = _traffic(w.name, "decode")
+    ceiling["decode_kernel_frac"] = round(ceiling["us"] / kernel_us, 4)
+    traffic = _traffic(w.name, "decode", kernel="decode_kernel")
     # the bound of the decode call: KV bytes at 8 TB/s against its MFMA work at the dense
     # peaks (2 x 512 FP8 QK + 2 x 512 FP8 PV + 2 x 64 BF16 RoPE FLOP per token and row)
     R = w.H * w.q_len
     t_hbm = kv_bytes / (HBM_PEAK_GBPS * 1e9) * 1e6
     t_mfma = w.total_tokens * R * (2 * 512 * 2 / (FP8_PEAK_TFLOPS * 1e12) + 2 * 64 / (BF16_PEAK_TFLOPS * 1e12)) * 1e6
-    kern = "snapmla_decode call (prep_kernel + decode_kernel), HIP events on its stream"
+    kern = ("decode_kernel alone (snapmla_debug_decode_kernel over the workspace a snapmla_decode call prepared), "
+            "HIP events on its stream")
+    call = {"what": "the whole snapmla_decode call (prep_kernel + decode_kernel), HIP events on its stream",
+            "us": round(decode_us, 2), "traffic": _traffic(w.name, "decode")}
     if t_mfma > t_hbm:
         fp8_eq = w.total_tokens * R * (2 * 512 * 2 + 2 * 64 * 2)      # BF16 FLOPs count twice at the FP8 rate
-        achieved = fp8_eq / (decode_us * 1e-6) / 1e12
-        roofline = {"bound": "mfma", "kernel": kern, "achieved": round(achieved, 1), "peak": FP8_PEAK_TFLOPS,
-                    "unit": "TFLOP/s (FP8-equivalent: BF16 FLOPs counted twice)",
+        achieved = fp8_eq / (kernel_us * 1e-6) / 1e12
+        call_achieved = fp8_eq / (decode_us * 1e-6) / 1e12
+        call.update(achieved=round(call_achieved, 1), frac=round(call_achieved / FP8_PEAK_TFLOPS, 4))
+        roofline = {"bound": "mfma", "kernel": kern, "kernel_us": round(kernel_us, 2), "achieved": round(achieved, 1),
+                    "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s (FP8-equivalent: BF16 FLOPs counted twice)",
                     "frac": round(achieved / FP8_PEAK_TFLOPS, 4), "traffic": traffic,
-                    "algorithmic_flops_per_launch": fp8_eq, "hbm_frac": round(decode_gbps / HBM_PEAK_GBPS, 4)}
+                    "algorithmic_flops_per_launch": fp8_eq, "hbm_frac": round(kernel_gbps / HBM_PEAK_GBPS, 4)}
     else:
-        roofline = {"bound": "hbm", "kernel": kern, "achieved": round(decode_gbps, 1), "peak": HBM_PEAK_GBPS,
-                    "unit": "GB/s", "frac": round(decode_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                    "algorithmic_bytes_per_launch": kv_bytes}
+        call.update(achieved=round(decode_gbps, 1), frac=round(decode_gbps / HBM_PEAK_GBPS, 4))
+        roofline = {"bound": "hbm", "kernel": kern, "kernel_us": round(kernel_us, 2), "achieved": round(kernel_gbps, 1),
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(kernel_gbps / HBM_PEAK_GBPS, 4),
+                    "traffic": traffic, "algorithmic_bytes_per_launch": kv_bytes}
+    roofline["decode_call"] = call
     roofline["read_ceiling"] = ceiling
     stream_ref["decode_call_frac"] = round(stream_ref["us"] / decode_us, 4)
+    stream_ref["decode_kernel_frac"] = round(stream_ref["us"] / kernel_us, 4)
     roofline["plain_stream"] = stream_ref
     line = {
         "metric": METRIC,

@@ -402,6 +402,25 @@ int snapmla_debug_read_ceiling(const uint8_t* kv_latent, const float* kv_scale, 
 int snapmla_debug_read_stream(const void* buf, int64_t bytes, int32_t grid, uint32_t* out, hipStream_t stream);
 
 /*
+ * snapmla_debug_decode_kernel -- measurement only: the decode launch of
+ * snapmla_decode (Algorithm 1 over the KV pieces) without its preparation launch,
+ * so that events around it time the decode kernel alone.  The workspace must hold
+ * what a snapmla_decode (or snapmla_append_decode) call with the same arguments,
+ * on the same stream, prepared: the quantized queries, the split plan and the
+ * start descriptors; the call then writes the same partials, direct rows and
+ * log-sum-exps as that call's decode launch.  Arguments, layouts, validation and
+ * status codes as snapmla_decode.
+ */
+int snapmla_debug_decode_kernel(const void* q_nope, const void* q_rope, const uint8_t* kv_latent,
+                                const float* kv_scale, const void* k_rope, const int32_t* page_table,
+                                const int32_t* seq_lens, int32_t B, int32_t q_len, int32_t H,
+                                int32_t max_pages, int32_t num_pages, int32_t page_size,
+                                float softmax_scale, int32_t causal, int32_t num_splits,
+                                int32_t kv_chunk_tokens, int32_t flags, void* workspace,
+                                size_t workspace_bytes, void* out, int32_t out_dtype, float* lse,
+                                hipStream_t stream);
+
+/*
  * snapmla_debug_mfma_fp8 -- test hook: the FP8 matrix-core dot product the decode's
  * QK content term is formed with (Section 3.1 runs that GEMM on FP8 matrix
  * cores).  For every tile t, one 16x16x128 FP8 MFMA from a zero accumulator:

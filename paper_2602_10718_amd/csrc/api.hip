@@ -73,7 +73,8 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
                   int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
                   float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
                   void* workspace, size_t workspace_bytes, void* out, int32_t out_dtype, float* lse,
-                  hipStream_t stream, bool bf16_cache, const AppendIn& app = AppendIn(), int32_t flags = 0) {
+                  hipStream_t stream, bool bf16_cache, const AppendIn& app = AppendIn(), int32_t flags = 0,
+                  bool run_prep = true) {
   int st = check_shapes(B, q_len, H, num_splits, kv_chunk_tokens);
   if (st != SNAPMLA_OK) return st;
   if ((flags & ~SNAPMLA_DECODE_EXACT_QK) != 0)
@@ -149,8 +150,10 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
     p.num_pages = num_pages;
     p.ablocks = (int)((app_toks + 3) / 4);
   }
-  hipError_t e = snapmla::launch_prep(p, stream);
-  if (e != hipSuccess) return hip_status(e, "decode prep launch");
+  if (run_prep) {
+    hipError_t e = snapmla::launch_prep(p, stream);
+    if (e != hipSuccess) return hip_status(e, "decode prep launch");
+  }
 
   snapmla::DecodeArgs d;
   d.q_nope = static_cast<const uint16_t*>(q_nope);
@@ -299,6 +302,17 @@ int snapmla_decode(const void* q_nope, const void* q_rope, const uint8_t* kv_lat
   return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
                        num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
                        workspace_bytes, out, out_dtype, lse, stream, false, AppendIn(), flags);
+}
+
+int snapmla_debug_decode_kernel(const void* q_nope, const void* q_rope, const uint8_t* kv_latent, const float* kv_scale,
+                                const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
+                                int32_t q_len, int32_t H, int32_t max_pages, int32_t num_pages, int32_t page_size,
+                                float softmax_scale, int32_t causal, int32_t num_splits, int32_t kv_chunk_tokens,
+                                int32_t flags, void* workspace, size_t workspace_bytes, void* out, int32_t out_dtype,
+                                float* lse, hipStream_t stream) {
+  return decode_common(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, B, q_len, H, max_pages,
+                       num_pages, page_size, softmax_scale, causal, num_splits, kv_chunk_tokens, workspace,
+                       workspace_bytes, out, out_dtype, lse, stream, false, AppendIn(), flags, false);
 }
 
 int snapmla_append_decode(const void* c_kv_new, const void* k_rope_new, int32_t n_new, const void* q_nope,

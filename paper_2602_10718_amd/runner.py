@@ -163,6 +163,15 @@ class DecodeRunner:
                           self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits, self.kv_chunk_tokens,
                           self.workspace, stream=stream, flags=self.flags, out=out, lse=lse)
 
+    def decode_kernel_only(self, stream=None):
+        """Measurement only: the decode launch of decode() alone, over the workspace the last decode() or
+        append_decode() prepared (FP8 cache)."""
+        out, lse = self._out()
+        sm.snapmla_debug_decode_kernel(self.q_nope, self.q_rope, self.kv_latent, self.kv_scale, self.k_rope,
+                                       self.page_table, self.seq_lens, self.wl.tau, self.wl.causal, self.num_splits,
+                                       self.kv_chunk_tokens, self.workspace, stream=stream, flags=self.flags, out=out,
+                                       lse=lse)
+
     def combine(self, stream=None):
         sm.snapmla_combine(self.workspace, self.seq_lens, self.B, self.q_len, self.H, self.num_splits,
                            self.kv_chunk_tokens, self.out, self.lse, stream=stream)

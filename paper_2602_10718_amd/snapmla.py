@@ -44,6 +44,8 @@ lib.snapmla_decode_workspace_size.argtypes = [_i32, _i32, _i32, _i32, _i32, ctyp
 lib.snapmla_decode.restype = ctypes.c_int
 lib.snapmla_decode.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
                                _i32, _i32, _p, _sz, _p, _i32, _p, _p]
+lib.snapmla_debug_decode_kernel.restype = ctypes.c_int
+lib.snapmla_debug_decode_kernel.argtypes = lib.snapmla_decode.argtypes
 lib.snapmla_combine.restype = ctypes.c_int
 lib.snapmla_combine.argtypes = [_p, _sz, _p, _i32, _i32, _i32, _i32, _i32, _p, _i32, _p, _p]
 lib.snapmla_e4m3_encode.restype = ctypes.c_int
@@ -76,7 +78,8 @@ EXPORTS = ["snapmla_abi_version", "snapmla_get_last_error", "snapmla_quantize_ap
            "snapmla_decode_workspace_size", "snapmla_decode", "snapmla_combine", "snapmla_e4m3_encode",
            "snapmla_fetch_dequant", "snapmla_quantize_cache_config", "snapmla_decode_bf16", "snapmla_append_bf16",
            "snapmla_debug_read_ceiling", "snapmla_append_decode", "snapmla_debug_set_spin_limit",
-           "snapmla_debug_mfma_fp8", "snapmla_debug_read_stream", "snapmla_append_decode_noalloc"]
+           "snapmla_debug_mfma_fp8", "snapmla_debug_read_stream", "snapmla_append_decode_noalloc",
+           "snapmla_debug_decode_kernel"]
 
 CACHE_CONFIGS = {"snapmla": 0, "A": 1, "B": 2, "C": 3, "D": 4}
 
@@ -180,6 +183,20 @@ def snapmla_decode(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_
                               page_size, float(softmax_scale), int(causal), num_splits, kv_chunk_tokens, int(flags),
                               _ptr(workspace), workspace.numel() * workspace.element_size(), *_out_args(out, lse),
                               _stream(stream)))
+
+
+def snapmla_debug_decode_kernel(q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens, softmax_scale,
+                                causal, num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None, flags=0,
+                                out=None, lse=None):
+    """Measurement only: snapmla_decode's decode launch alone, over a workspace that a snapmla_decode (or
+    snapmla_append_decode) call with the same arguments prepared on the same stream."""
+    B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
+    _check(lib.snapmla_debug_decode_kernel(_ptr(q_nope), _ptr(q_rope), _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope),
+                                           _ptr(page_table), _ptr(seq_lens), B, q_len, H, page_table.shape[1],
+                                           kv_latent.shape[0], page_size, float(softmax_scale), int(causal), num_splits,
+                                           kv_chunk_tokens, int(flags), _ptr(workspace),
+                                           workspace.numel() * workspace.element_size(), *_out_args(out, lse),
+                                           _stream(stream)))
 
 
 def snapmla_append_decode(c_kv_new, k_rope_new, q_nope, q_rope, kv_latent, kv_scale, k_rope, page_table, seq_lens,

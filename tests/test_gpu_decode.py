@@ -154,6 +154,28 @@ def test_plan_with_many_sequences_and_units():
             check_sequence(run, b, reference(w, b, qn, qr), label=f"many-seq {kw}")
 
 
+@pytest.mark.parametrize("name", ["ragged-h16", "h128-two-rowgroups", "fixed-chunks-causal"])
+def test_decode_kernel_alone_repeats_the_decode_launch(name):
+    """snapmla_debug_decode_kernel, the decode launch alone that bench.py times for the roofline, over the
+    workspace a snapmla_decode call prepared: after it and the combine, every output row and LSE equals the
+    full call's bit for bit (direct rows included: the outputs are overwritten with a marker in between)."""
+    fac, kw = CASES[name]
+    w = fac()
+    run = runner(w, **kw)
+    print(f"[decode kernel alone] {name}", flush=True)
+    run.decode()
+    run.combine()
+    torch.cuda.synchronize()
+    out1, lse1 = run.out.clone(), run.lse.clone()
+    run.out.fill_(12345.0)
+    run.lse.fill_(12345.0)
+    run.decode_kernel_only()
+    run.combine()
+    torch.cuda.synchronize()
+    assert torch.equal(run.out.view(torch.int32), out1.view(torch.int32))
+    assert torch.equal(run.lse.view(torch.int32), lse1.view(torch.int32))
+
+
 @pytest.mark.parametrize("splits", [600, 1024, 1500])
 def test_padded_plan_with_more_parts_than_positions(splits):
     """The balanced plan of a one-row-group launch charges each sequence start 4 virtual
