@@ -73,13 +73,16 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(CombineArgs a) {
   auto pid = [&](int i) { return P.pid(i); };
 
   // pass 1: lane i reads the log-sum-exp of candidate piece first + i (64 at a
-  // time), the wave reduces the maximum and NaN flag
+  // time), the wave reduces the maximum and NaN flag; the first 64 stay in x0 for
+  // pass 2
   float M = -INFINITY;
   bool anynan = false;
+  float x0 = -INFINITY;
   for (int i0 = first; i0 <= last; i0 += 64) {
     const int i = i0 + lane;
     float x = -INFINITY;
     if (i <= last && exists(i)) x = a.part_lse[pid(i) * a.rows_pad + r];
+    if (i0 == first) x0 = x;
     anynan |= x != x;
     M = fmaxf(M, x);
   }
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(CombineArgs a) {
       const int i = i0 + lane;
       float wi = 0.0f;
       if (i <= last && exists(i)) {
-        const float x = a.part_lse[pid(i) * a.rows_pad + r];
+        const float x = i0 == first ? x0 : a.part_lse[pid(i) * a.rows_pad + r];
         wi = x > -INFINITY ? expf(x - M) : 0.0f;
       }
       S += wi;
