@@ -409,7 +409,11 @@ int snapmla_debug_read_stream(const void* buf, int64_t bytes, int32_t grid, uint
  * on the same stream, prepared: the quantized queries, the split plan and the
  * start descriptors; the call then writes the same partials, direct rows and
  * log-sum-exps as that call's decode launch.  Arguments, layouts, validation and
- * status codes as snapmla_decode.
+ * status codes as snapmla_decode; in addition, SNAPMLA_INVALID_ARGUMENT when the
+ * last preparation written into this workspace was not an FP8 decode call with the
+ * same q_nope and seq_lens buffers, B, q_len, H, num_splits and kv_chunk_tokens
+ * (the library records each preparation launch per workspace; the buffers'
+ * contents and the stream order are not checked).
  */
 int snapmla_debug_decode_kernel(const void* q_nope, const void* q_rope, const uint8_t* kv_latent,
                                 const float* kv_scale, const void* k_rope, const int32_t* page_table,

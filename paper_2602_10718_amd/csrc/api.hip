@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <mutex>
 #include <string>
+#include <unordered_map>
 
 #include "snapmla.h"
 #include "snapmla_internal.h"
@@ -67,6 +68,26 @@ struct AppendIn {
   const void* k_rope_new = nullptr;
   int32_t n_new = 0;
 };
+
+// What the last FP8 preparation launch into each workspace was made from.  The decode
+// launch alone (snapmla_debug_decode_kernel) reads the start descriptors, block prefix
+// and quantized queries that launch wrote; with a workspace no matching call prepared
+// those words are undefined and the kernel could address pages out of bounds, so the
+// entry point refuses it on the host.  (Only the buffers and sizes are compared: keeping
+// the contents of seq_lens and q_nope unchanged, and ordering the launch after the
+// preparation, stay the caller's part.)
+struct PrepKey {
+  const void* q_nope = nullptr;
+  const int32_t* seq_lens = nullptr;
+  int32_t B = 0, q_len = 0, H = 0, num_splits = 0, kv_chunk_tokens = 0;
+  bool operator==(const PrepKey& o) const {
+    return q_nope == o.q_nope && seq_lens == o.seq_lens && B == o.B && q_len == o.q_len &&
+           H == o.H && num_splits == o.num_splits && kv_chunk_tokens == o.kv_chunk_tokens;
+  }
+};
+std::mutex g_prep_mu;
+std::unordered_map<const void*, PrepKey> g_prepared;   // workspace -> its last FP8 preparation
+constexpr size_t kMaxPreparedRecords = 4096;           // bounded: cleared when full
 
 int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent, const float* kv_scale,
                   const void* k_rope, const int32_t* page_table, const int32_t* seq_lens, int32_t B,
@@ -150,9 +171,30 @@ int decode_common(const void* q_nope, const void* q_rope, const void* kv_latent,
     p.num_pages = num_pages;
     p.ablocks = (int)((app_toks + 3) / 4);
   }
+  PrepKey key;
+  key.q_nope = q_nope;
+  key.seq_lens = seq_lens;
+  key.B = B;
+  key.q_len = q_len;
+  key.H = H;
+  key.num_splits = num_splits;
+  key.kv_chunk_tokens = kv_chunk_tokens;
   if (run_prep) {
     hipError_t e = snapmla::launch_prep(p, stream);
     if (e != hipSuccess) return hip_status(e, "decode prep launch");
+    std::lock_guard<std::mutex> lk(g_prep_mu);
+    if (bf16_cache) {
+      g_prepared.erase(workspace);
+    } else {
+      if (g_prepared.size() >= kMaxPreparedRecords) g_prepared.clear();
+      g_prepared[workspace] = key;
+    }
+  } else {
+    std::lock_guard<std::mutex> lk(g_prep_mu);
+    auto it = g_prepared.find(workspace);
+    if (bf16_cache || it == g_prepared.end() || !(it->second == key))
+      return fail(SNAPMLA_INVALID_ARGUMENT,
+                  "workspace not prepared by an FP8 decode call with these queries, lengths and sizes");
   }
 
   snapmla::DecodeArgs d;

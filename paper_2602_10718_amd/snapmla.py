@@ -189,7 +189,8 @@ def snapmla_debug_decode_kernel(q_nope, q_rope, kv_latent, kv_scale, k_rope, pag
                                 causal, num_splits, kv_chunk_tokens, workspace, page_size=64, stream=None, flags=0,
                                 out=None, lse=None):
     """Measurement only: snapmla_decode's decode launch alone, over a workspace that a snapmla_decode (or
-    snapmla_append_decode) call with the same arguments prepared on the same stream."""
+    snapmla_append_decode) call with the same arguments prepared on the same stream (a workspace that no
+    matching FP8 call prepared last is refused with SnapMLAError)."""
     B, q_len, H = q_nope.shape[0], q_nope.shape[1], q_nope.shape[2]
     _check(lib.snapmla_debug_decode_kernel(_ptr(q_nope), _ptr(q_rope), _ptr(kv_latent), _ptr(kv_scale), _ptr(k_rope),
                                            _ptr(page_table), _ptr(seq_lens), B, q_len, H, page_table.shape[1],

@@ -108,6 +108,20 @@ def test_decode_argument_errors_before_any_launch(sm):
                             None) == 0
 
 
+def test_decode_kernel_alone_refuses_an_unprepared_workspace(sm):
+    """snapmla_debug_decode_kernel reads the start descriptors a preparation launch wrote; a workspace
+    that no FP8 decode call with the same buffers and sizes prepared is refused on the host, before any
+    launch (the pointers below are never dereferenced)."""
+    L = sm.lib
+    st = L.snapmla_debug_decode_kernel(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0,
+                                       4096, 1 << 30, None, 0, None, None)
+    assert st == 1 and "not prepared" in sm.snapmla_get_last_error()
+    # the ordinary argument checks still come first
+    st = L.snapmla_debug_decode_kernel(4096, 4096, 4096, 4096, 4096, 4096, 4096, 2, 1, 16, 4, 8, 64, 0.1, 0, 8, 0, 0,
+                                       4096, 16, None, 0, None, None)
+    assert st == 3
+
+
 def test_other_entry_points_validate(sm):
     L = sm.lib
     assert L.snapmla_quantize_append(None, None, None, None, 1, 1, 4, 4, 32, None, None, None, None) == 2

@@ -176,6 +176,34 @@ def test_decode_kernel_alone_repeats_the_decode_launch(name):
     assert torch.equal(run.lse.view(torch.int32), lse1.view(torch.int32))
 
 
+def test_decode_kernel_alone_needs_a_matching_preparation():
+    """The decode launch alone is refused for a workspace that no FP8 decode call prepared, or that one
+    with other sizes prepared last, and accepted again once a matching call has prepared it."""
+    fac, kw = CASES["ragged-h16"]
+    w = fac()
+    from paper_2602_10718_amd import snapmla as sm
+    run = runner(w, **kw)
+    print("[decode kernel alone: preparation check]", flush=True)
+    run.decode()
+    run.combine()
+    torch.cuda.synchronize()
+    out1 = run.out.clone()
+    fresh = torch.zeros_like(run.workspace)
+    with pytest.raises(RuntimeError, match="not prepared"):
+        sm.snapmla_debug_decode_kernel(run.q_nope, run.q_rope, run.kv_latent, run.kv_scale, run.k_rope,
+                                       run.page_table, run.seq_lens, w.tau, w.causal, run.num_splits,
+                                       run.kv_chunk_tokens, fresh)
+    with pytest.raises(RuntimeError, match="not prepared"):
+        sm.snapmla_debug_decode_kernel(run.q_nope, run.q_rope, run.kv_latent, run.kv_scale, run.k_rope,
+                                       run.page_table, run.seq_lens, w.tau, w.causal, run.num_splits // 2,
+                                       run.kv_chunk_tokens, run.workspace)
+    run.out.fill_(12345.0)
+    run.decode_kernel_only()
+    run.combine()
+    torch.cuda.synchronize()
+    assert torch.equal(run.out.view(torch.int32), out1.view(torch.int32))
+
+
 @pytest.mark.parametrize("splits", [600, 1024, 1500])
 def test_padded_plan_with_more_parts_than_positions(splits):
     """The balanced plan of a one-row-group launch charges each sequence start 4 virtual
